@@ -1,0 +1,192 @@
+/*
+ * entropyinfer.h -- C ABI of libentropyinfer.so, the MI355X (gfx950) prefill
+ * hot path of EntropyInfer ("From Rigid to Dynamic: Entropy-Guided Adaptive
+ * Inference for Long-Context LLMs"):
+ *
+ *   ei_entropy_probe        Algorithms 1-2 and the row entropy (Section 4.2)
+ *   ei_select_blocks        Algorithm 3 (rigid / dynamic heads, budgets) and
+ *                           per-segment top-k key-block selection (Section 4.2,
+ *                           Appendix A Eq. t_topk)
+ *   ei_sparse_prefill_attn  causal GQA attention over the selected blocks
+ *                           (Appendix A Eq. t_spa)
+ *   ei_dense_prefill_attn   dense (causal) GQA attention, the full-attention
+ *                           baseline the paper compares against
+ *
+ * Conventions shared by every entry point
+ *  - Tensors are contiguous, row-major, in device memory owned by the caller;
+ *    the library never allocates, frees or keeps a pointer after returning.
+ *  - bf16 tensors are passed as uint16_t bit patterns.
+ *  - Q is [B][Hq][N][D], K and V are [B][Hkv][N][D]; query head h reads key
+ *    head h / (Hq / Hkv) (grouped-query attention).  D must be 128.
+ *  - Segment size L_S and block size L_B (Section 4.1): L_B is 64 or 128,
+ *    L_S is a multiple of 128 and of L_B.  C_S = ceil(N / L_S) segments,
+ *    C_B = ceil(N / L_B) key blocks, r = L_S / L_B.  A ragged tail (N not a
+ *    multiple of L_S) forms a short last segment / block.
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Calls are
+ *    asynchronous; outputs are valid once the stream is synchronised.
+ *  - Every argument is validated on the host before anything is launched; a
+ *    failed check returns a negative ei_status and launches nothing.
+ *    B == 0 or N == 0 is valid and launches nothing.
+ *  - Outputs must not alias inputs.  Identical inputs give bitwise-identical
+ *    outputs (no atomics in any reduction).  No global state, no logging;
+ *    calls on different streams may run concurrently.
+ */
+#ifndef ENTROPYINFER_H
+#define ENTROPYINFER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  EI_OK = 0,
+  EI_ERR_NULL = -1,        /* a required pointer is NULL */
+  EI_ERR_SHAPE = -2,       /* inconsistent or out-of-range sizes */
+  EI_ERR_UNSUPPORTED = -3, /* valid but not implemented here (e.g. D != 128) */
+  EI_ERR_WORKSPACE = -4,   /* workspace missing or smaller than required */
+  EI_ERR_LAUNCH = -5       /* a kernel launch failed (hipGetLastError) */
+} ei_status;
+
+/* Problem sizes: batch B, query heads Hq, key/value heads Hkv, sequence N,
+ * head dimension D. */
+typedef struct {
+  int32_t batch, n_q_heads, n_kv_heads, seq_len, head_dim;
+} ei_dims;
+
+/* Segment size L_S and key-block size L_B (Section 4.1). */
+typedef struct {
+  int32_t seg_len, block_len;
+} ei_tiling;
+
+/* Algorithm 3's constants, exposed as parameters: entropy threshold e_t
+ * (1e-5), budget coefficient alpha (0.5), fluctuation threshold Delta_t
+ * (0.4), base budget B_h in tokens (2048, Section 5.1.3) and the cap
+ * multiplier (3: B_i <= 3 B_h, Appendix A). */
+typedef struct {
+  float entropy_threshold;
+  double alpha;
+  double delta_t;
+  int32_t base_budget_tokens;
+  int32_t max_budget_mult;
+} ei_budget_params;
+
+/* Version of this interface (incremented on any change of a signature). */
+int32_t ei_abi_version(void);
+
+/* Human-readable name of a status code (static storage). */
+const char* ei_status_str(ei_status status);
+
+/* C_S = ceil(N / L_S) and C_B = ceil(N / L_B); -1 on invalid sizes. */
+int64_t ei_num_segments(ei_dims dims, ei_tiling tiling);
+int64_t ei_num_blocks(ei_dims dims, ei_tiling tiling);
+
+/* Entries per (b, h, s) row of the selection lists:
+ * floor(mult * B_h / L_B) + L_S / L_B; -1 on invalid parameters. */
+int32_t ei_kmax(ei_tiling tiling, ei_budget_params params);
+
+/* Workspace bytes ei_entropy_probe needs (Q representation in binary64 and
+ * K representation in bf16, Algorithm 1); 0 on invalid sizes. */
+size_t ei_probe_workspace_bytes(ei_dims dims, ei_tiling tiling);
+
+/*
+ * ei_entropy_probe -- Algorithms 1 and 2 and the row entropy (Section 4.2).
+ *
+ * For query head h, segment s and visible key block j < n_vis(s) =
+ * min((s+1) r, C_B) (block-causal, including the segment's own blocks):
+ * Q_max / Q_min are the element-wise max / min of the segment's query rows,
+ * K_max / K_min those of the block's key rows (Algorithm 1); the four logits
+ * x_ab = probe_scale * <Q_a, K_b> are computed in binary64 (exact for bf16
+ * products); S1..S4 are their softmaxes over j; A = max((S1 + S2) / 2,
+ * (S3 + S4) / 2) (Algorithm 2, used without renormalisation); the entropy is
+ * -sum_j A ln A (natural log, Section 3).
+ *
+ *   q, k         bf16 [B][Hq][N][D], [B][Hkv][N][D]
+ *   probe_scale  multiplies the logits; 1.0 is Algorithm 2 as printed
+ *   log_scores   out, fp32 [B][Hq][C_S][C_B]: ln A for j < n_vis(s); entries
+ *                with j >= n_vis(s) are left untouched
+ *   entropy      out, fp32 [B][Hq][C_S]
+ *   workspace    device scratch of at least ei_probe_workspace_bytes()
+ *
+ * Errors: EI_ERR_NULL, EI_ERR_SHAPE, EI_ERR_UNSUPPORTED (D != 128, or C_B too
+ * large for one workgroup's LDS), EI_ERR_WORKSPACE, EI_ERR_LAUNCH.
+ */
+ei_status ei_entropy_probe(const uint16_t* q, const uint16_t* k, ei_dims dims,
+                           ei_tiling tiling, double probe_scale, float* log_scores,
+                           float* entropy, void* workspace, size_t workspace_bytes,
+                           void* stream);
+
+/*
+ * ei_select_blocks -- head classification, budget allocation (Algorithm 3)
+ * and top-k block selection (Section 4.2).
+ *
+ * Head (b, h) is rigid iff every entropy[b][h][s] < e_t; a NaN entropy makes
+ * it dynamic.  Budgets in tokens, binary64, no FMA contraction: rigid
+ * B_s = B_h; dynamic B_0 = B_h and B_s = clamp(B_{s-1} + (alpha B_h) *
+ * (|e_s - e_{s-1}| / e_{s-1} - Delta_t), B_h, mult B_h) with 0/0 -> 0,
+ * x/0 -> +inf and NaN -> B_h.  k_s = min(floor(B_s / L_B), s r) past blocks
+ * are kept: those with the largest log_scores (binary32 total order, NaN
+ * lowest, -0 == +0, equal scores -> higher block index), plus the segment's
+ * own blocks s r .. min((s+1) r, C_B) - 1, which are not charged.
+ *
+ *   log_scores, entropy  fp32 as written by ei_entropy_probe (only
+ *                        j < s r is read)
+ *   kmax                 entries per row, >= ei_kmax(tiling, params)
+ *   head_is_rigid        out, u8 [B][Hq]
+ *   budget_blocks        out, i32 [B][Hq][C_S] = k_s
+ *   block_idx            out, i32 [B][Hq][C_S][kmax], strictly ascending,
+ *                        padded with -1
+ *   block_cnt            out, i32 [B][Hq][C_S] = k_s + own blocks
+ *
+ * Errors: EI_ERR_NULL, EI_ERR_SHAPE (including kmax too small or a negative
+ * budget), EI_ERR_UNSUPPORTED (C_B beyond the selector's register tile),
+ * EI_ERR_LAUNCH.
+ */
+ei_status ei_select_blocks(const float* log_scores, const float* entropy, ei_dims dims,
+                           ei_tiling tiling, ei_budget_params params, int32_t kmax,
+                           uint8_t* head_is_rigid, int32_t* budget_blocks,
+                           int32_t* block_idx, int32_t* block_cnt, void* stream);
+
+/*
+ * ei_sparse_prefill_attn -- block-sparse causal GQA attention (Section 4.2,
+ * Appendix A Eq. t_spa).  Query i of segment s attends to the keys of the
+ * blocks block_idx[b][h][s][0 .. block_cnt) that are <= i:
+ * O_i = sum_j softmax_j(softmax_scale <q_i, k_j>) v_j, fp32 accumulation and
+ * online softmax, bf16 output.
+ *
+ *   q, k, v        bf16 [B][Hq][N][D], [B][Hkv][N][D], [B][Hkv][N][D]
+ *   softmax_scale  usually 1 / sqrt(D)
+ *   block_idx      i32 [B][Hq][C_S][kmax] strictly ascending block indices
+ *   block_cnt      i32 [B][Hq][C_S]
+ *   o              out, bf16 [B][Hq][N][D]
+ *
+ * A list is read up to block_cnt (clamped to [0, kmax]) and stops at the
+ * first entry that is negative, >= C_B or not above its predecessor, so a
+ * malformed list never leads to an out-of-bounds access.  A query with no
+ * visible key gets a zero row.
+ *
+ * Errors: EI_ERR_NULL, EI_ERR_SHAPE, EI_ERR_UNSUPPORTED, EI_ERR_LAUNCH.
+ */
+ei_status ei_sparse_prefill_attn(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                                 ei_dims dims, ei_tiling tiling, float softmax_scale,
+                                 const int32_t* block_idx, const int32_t* block_cnt,
+                                 int32_t kmax, uint16_t* o, void* stream);
+
+/*
+ * ei_dense_prefill_attn -- dense GQA attention (Section 2's A_h V), causal
+ * (keys j <= i) when `causal` is non-zero, else over all N keys; same tile
+ * code and numerics as ei_sparse_prefill_attn.
+ *
+ * Errors: EI_ERR_NULL, EI_ERR_SHAPE, EI_ERR_UNSUPPORTED, EI_ERR_LAUNCH.
+ */
+ei_status ei_dense_prefill_attn(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                                ei_dims dims, float softmax_scale, int32_t causal,
+                                uint16_t* o, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ENTROPYINFER_H */

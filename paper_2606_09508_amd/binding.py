@@ -1,0 +1,257 @@
+"""Python binding of libentropyinfer.so (argument marshalling only).
+
+Every function takes torch tensors that already live on a ROCm device, checks
+dtype / shape / contiguity, and passes raw device pointers plus the current
+HIP stream to the C ABI of the same name (``include/entropyinfer.h``).  All
+arithmetic runs in the library's HIP kernels; there is no fallback: if the
+library is missing or a call fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libentropyinfer.so")
+
+EI_OK = 0
+_STATUS = {0: "EI_OK", -1: "EI_ERR_NULL", -2: "EI_ERR_SHAPE", -3: "EI_ERR_UNSUPPORTED",
+           -4: "EI_ERR_WORKSPACE", -5: "EI_ERR_LAUNCH"}
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("seq_len", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32)]
+
+
+class Tiling(ctypes.Structure):
+    _fields_ = [("seg_len", ctypes.c_int32), ("block_len", ctypes.c_int32)]
+
+
+class BudgetParams(ctypes.Structure):
+    _fields_ = [("entropy_threshold", ctypes.c_float), ("alpha", ctypes.c_double),
+                ("delta_t", ctypes.c_double), ("base_budget_tokens", ctypes.c_int32),
+                ("max_budget_mult", ctypes.c_int32)]
+
+
+class EIError(RuntimeError):
+    def __init__(self, fn: str, status: int, text: str):
+        super().__init__(f"{fn} returned {status} ({_STATUS.get(status, '?')}): {text}")
+        self.status = status
+
+
+_LIB = None
+_VP = ctypes.c_void_p
+
+
+def lib() -> ctypes.CDLL:
+    """Load libentropyinfer.so (built in-tree by ``build.py``); raise if absent."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run paper_2606_09508_amd/build.py "
+                               "(or __graft_entry__.build()) first")
+        L = ctypes.CDLL(LIB_PATH)
+        L.ei_abi_version.restype = ctypes.c_int32
+        L.ei_status_str.restype = ctypes.c_char_p
+        L.ei_status_str.argtypes = [ctypes.c_int]
+        L.ei_num_segments.restype = ctypes.c_int64
+        L.ei_num_segments.argtypes = [Dims, Tiling]
+        L.ei_num_blocks.restype = ctypes.c_int64
+        L.ei_num_blocks.argtypes = [Dims, Tiling]
+        L.ei_kmax.restype = ctypes.c_int32
+        L.ei_kmax.argtypes = [Tiling, BudgetParams]
+        L.ei_probe_workspace_bytes.restype = ctypes.c_size_t
+        L.ei_probe_workspace_bytes.argtypes = [Dims, Tiling]
+        L.ei_entropy_probe.restype = ctypes.c_int
+        L.ei_entropy_probe.argtypes = [_VP, _VP, Dims, Tiling, ctypes.c_double, _VP, _VP, _VP,
+                                       ctypes.c_size_t, _VP]
+        L.ei_select_blocks.restype = ctypes.c_int
+        L.ei_select_blocks.argtypes = [_VP, _VP, Dims, Tiling, BudgetParams, ctypes.c_int32, _VP,
+                                       _VP, _VP, _VP, _VP]
+        L.ei_sparse_prefill_attn.restype = ctypes.c_int
+        L.ei_sparse_prefill_attn.argtypes = [_VP, _VP, _VP, Dims, Tiling, ctypes.c_float, _VP,
+                                             _VP, ctypes.c_int32, _VP, _VP]
+        L.ei_dense_prefill_attn.restype = ctypes.c_int
+        L.ei_dense_prefill_attn.argtypes = [_VP, _VP, _VP, Dims, ctypes.c_float, ctypes.c_int32,
+                                            _VP, _VP]
+        _LIB = L
+    return _LIB
+
+
+def _check(fn: str, st: int) -> None:
+    if st != EI_OK:
+        raise EIError(fn, st, lib().ei_status_str(st).decode())
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(t: torch.Tensor):
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _req(t: torch.Tensor, name: str, dtype, ndim: int) -> None:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on a ROCm device, got {t.device}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.dim() != ndim or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous {ndim}-d tensor, got {tuple(t.shape)}")
+
+
+def dims_of(q: torch.Tensor, k: torch.Tensor) -> Dims:
+    B, Hq, N, D = q.shape
+    return Dims(B, Hq, k.shape[1], N, D)
+
+
+def budget_params(e_t: float = 1e-5, alpha: float = 0.5, delta_t: float = 0.4,
+                  base_budget: int = 2048, mult: int = 3) -> BudgetParams:
+    return BudgetParams(float(e_t), float(alpha), float(delta_t), int(base_budget), int(mult))
+
+
+def num_segments(N: int, seg_len: int) -> int:
+    return -(-N // seg_len)
+
+
+def num_blocks(N: int, block_len: int) -> int:
+    return -(-N // block_len)
+
+
+def kmax(seg_len: int, block_len: int, base_budget: int = 2048, mult: int = 3) -> int:
+    v = lib().ei_kmax(Tiling(seg_len, block_len), budget_params(base_budget=base_budget, mult=mult))
+    if v < 0:
+        raise ValueError("invalid tiling or budget parameters")
+    return v
+
+
+def probe_workspace_bytes(dims: Dims, seg_len: int, block_len: int) -> int:
+    return int(lib().ei_probe_workspace_bytes(dims, Tiling(seg_len, block_len)))
+
+
+def entropy_probe(q, k, seg_len: int, block_len: int, probe_scale: float = 1.0,
+                  log_scores=None, entropy=None, workspace=None):
+    """ei_entropy_probe: returns (log_scores fp32 [B,Hq,C_S,C_B], entropy fp32 [B,Hq,C_S])."""
+    _req(q, "q", torch.bfloat16, 4)
+    _req(k, "k", torch.bfloat16, 4)
+    d = dims_of(q, k)
+    CS, CB = num_segments(d.seq_len, seg_len), num_blocks(d.seq_len, block_len)
+    dev = q.device
+    if log_scores is None:
+        log_scores = torch.empty((d.batch, d.n_q_heads, CS, CB), dtype=torch.float32, device=dev)
+    if entropy is None:
+        entropy = torch.empty((d.batch, d.n_q_heads, CS), dtype=torch.float32, device=dev)
+    _req(log_scores, "log_scores", torch.float32, 4)
+    _req(entropy, "entropy", torch.float32, 3)
+    if tuple(log_scores.shape) != (d.batch, d.n_q_heads, CS, CB) or \
+            tuple(entropy.shape) != (d.batch, d.n_q_heads, CS):
+        raise ValueError("log_scores / entropy have the wrong shape")
+    need = probe_workspace_bytes(d, seg_len, block_len)
+    if workspace is None:
+        workspace = torch.empty((max(need, 1),), dtype=torch.uint8, device=dev)
+    _check("ei_entropy_probe",
+           lib().ei_entropy_probe(_ptr(q), _ptr(k), d, Tiling(seg_len, block_len),
+                                  float(probe_scale), _ptr(log_scores), _ptr(entropy),
+                                  _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                  _stream(q)))
+    return log_scores, entropy
+
+
+def select_blocks(log_scores, entropy, seq_len: int, seg_len: int, block_len: int,
+                  e_t: float = 1e-5, alpha: float = 0.5, delta_t: float = 0.4,
+                  base_budget: int = 2048, mult: int = 3, kmax_: int | None = None,
+                  head_dim: int = 128, n_kv_heads: int | None = None, out: dict | None = None):
+    """ei_select_blocks: returns dict(rigid u8 [B,Hq], budget i32 [B,Hq,C_S],
+    idx i32 [B,Hq,C_S,kmax], cnt i32 [B,Hq,C_S])."""
+    _req(log_scores, "log_scores", torch.float32, 4)
+    _req(entropy, "entropy", torch.float32, 3)
+    B, Hq, CS, CB = log_scores.shape
+    p = budget_params(e_t, alpha, delta_t, base_budget, mult)
+    km = kmax(seg_len, block_len, base_budget, mult) if kmax_ is None else int(kmax_)
+    dev = log_scores.device
+    if out is None:
+        out = {"rigid": torch.empty((B, Hq), dtype=torch.uint8, device=dev),
+               "budget": torch.empty((B, Hq, CS), dtype=torch.int32, device=dev),
+               "idx": torch.empty((B, Hq, CS, km), dtype=torch.int32, device=dev),
+               "cnt": torch.empty((B, Hq, CS), dtype=torch.int32, device=dev)}
+    _req(out["rigid"], "rigid", torch.uint8, 2)
+    _req(out["budget"], "budget", torch.int32, 3)
+    _req(out["idx"], "idx", torch.int32, 4)
+    _req(out["cnt"], "cnt", torch.int32, 3)
+    if out["idx"].shape[-1] != km:
+        raise ValueError("idx last dimension must equal kmax")
+    d = Dims(B, Hq, Hq if n_kv_heads is None else n_kv_heads, seq_len, head_dim)
+    _check("ei_select_blocks",
+           lib().ei_select_blocks(_ptr(log_scores), _ptr(entropy), d, Tiling(seg_len, block_len),
+                                  p, km, _ptr(out["rigid"]), _ptr(out["budget"]),
+                                  _ptr(out["idx"]), _ptr(out["cnt"]), _stream(log_scores)))
+    return out
+
+
+def sparse_prefill_attn(q, k, v, block_idx, block_cnt, seg_len: int, block_len: int,
+                        softmax_scale: float | None = None, out=None):
+    """ei_sparse_prefill_attn: bf16 [B,Hq,N,D] output."""
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _req(t, n, torch.bfloat16, 4)
+    _req(block_idx, "block_idx", torch.int32, 4)
+    _req(block_cnt, "block_cnt", torch.int32, 3)
+    d = dims_of(q, k)
+    if out is None:
+        out = torch.empty_like(q)
+    _req(out, "out", torch.bfloat16, 4)
+    if k.shape != v.shape or tuple(out.shape) != tuple(q.shape):
+        raise ValueError("k / v / out shapes do not match q")
+    CS = num_segments(d.seq_len, seg_len)
+    if tuple(block_idx.shape[:3]) != (d.batch, d.n_q_heads, CS) or \
+            tuple(block_cnt.shape) != (d.batch, d.n_q_heads, CS):
+        raise ValueError("block_idx / block_cnt do not match [B, Hq, C_S]")
+    sc = 1.0 / math.sqrt(d.head_dim) if softmax_scale is None else float(softmax_scale)
+    _check("ei_sparse_prefill_attn",
+           lib().ei_sparse_prefill_attn(_ptr(q), _ptr(k), _ptr(v), d, Tiling(seg_len, block_len),
+                                        sc, _ptr(block_idx), _ptr(block_cnt),
+                                        int(block_idx.shape[-1]), _ptr(out), _stream(q)))
+    return out
+
+
+def dense_prefill_attn(q, k, v, softmax_scale: float | None = None, causal: bool = True,
+                       out=None):
+    """ei_dense_prefill_attn: bf16 [B,Hq,N,D] output."""
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _req(t, n, torch.bfloat16, 4)
+    d = dims_of(q, k)
+    if out is None:
+        out = torch.empty_like(q)
+    _req(out, "out", torch.bfloat16, 4)
+    if k.shape != v.shape or tuple(out.shape) != tuple(q.shape):
+        raise ValueError("k / v / out shapes do not match q")
+    sc = 1.0 / math.sqrt(d.head_dim) if softmax_scale is None else float(softmax_scale)
+    _check("ei_dense_prefill_attn",
+           lib().ei_dense_prefill_attn(_ptr(q), _ptr(k), _ptr(v), d, sc, 1 if causal else 0,
+                                       _ptr(out), _stream(q)))
+    return out
+
+
+def entropy_guided_prefill(q, k, v, seg_len: int = 128, block_len: int = 64,
+                           base_budget: int = 2048, e_t: float = 1e-5, alpha: float = 0.5,
+                           delta_t: float = 0.4, mult: int = 3, probe_scale: float = 1.0,
+                           softmax_scale: float | None = None, bufs: dict | None = None):
+    """The whole hot path on one layer: probe -> select -> sparse attention.
+
+    ``bufs`` (optional) caches the intermediate device buffers between calls.
+    Returns (output, selection dict, log_scores, entropy).
+    """
+    bufs = {} if bufs is None else bufs
+    ls, en = entropy_probe(q, k, seg_len, block_len, probe_scale, bufs.get("log_scores"),
+                           bufs.get("entropy"), bufs.get("workspace"))
+    sel = select_blocks(ls, en, q.shape[2], seg_len, block_len, e_t, alpha, delta_t, base_budget,
+                        mult, n_kv_heads=k.shape[1], out=bufs.get("sel"))
+    o = sparse_prefill_attn(q, k, v, sel["idx"], sel["cnt"], seg_len, block_len, softmax_scale,
+                            bufs.get("out"))
+    return o, sel, ls, en

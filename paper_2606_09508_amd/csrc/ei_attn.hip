@@ -1,0 +1,300 @@
+// Causal GQA prefill attention on bf16 MFMA (gfx950), block-sparse over the
+// selected key blocks (Section 4.2, Appendix A Eq. t_spa) or dense (the
+// full-attention baseline).
+//
+// One workgroup = one 128-row query tile of one (batch, query head); four
+// waves own 32 query rows each.  Keys are visited in 64-key sub-blocks staged
+// through LDS (K row-major, V transposed); per sub-block each wave computes
+//   S^T = K Q^T        2 x 8  MFMA 32x32x16 (keys on M, queries on N)
+//   online softmax     fp32, base 2, the row of one query lives in one lane
+//                      pair (lanes l and l^32)
+//   O^T += V^T P^T     4 x 4  MFMA 32x32x16 (head dims on M)
+// With keys on the M dimension every lane owns one query's scores, so the
+// softmax needs a single cross-lane exchange per sub-block, and the output
+// rescale uses the lane's own running maximum.
+//
+// MFMA 32x32x16 bf16 operand layout (lane l, half h = l / 32):
+//   A[i][k]: lane holds i = l % 32, k = 8h .. 8h+7
+//   B[k][j]: lane holds j = l % 32, k = 8h .. 8h+7
+//   D[i][j]: lane holds j = l % 32, i = 8 (r / 4) + 4h + r % 4, r = 0..15
+// The keys of the S^T output a lane holds are therefore not contiguous; V is
+// stored in LDS with the matching key permutation so that P^T can be fed to
+// the second product straight from registers.
+//
+// Workgroups are mapped so that each XCD (dispatched round-robin) receives a
+// contiguous run of (batch, KV head, tile, query head) work: the G query
+// heads that share a K/V head, and neighbouring tiles, run on one XCD and
+// reuse K/V blocks from its L2.  Heavier (later) tiles are issued first.
+#include "ei_internal.h"
+
+#include <math.h>
+
+namespace ei {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kThreads = 256;
+constexpr int kTileQ = 128;
+constexpr int kSub = 64;            // keys per staged sub-block
+constexpr int kKStride = 136;       // K row stride in LDS (bf16), padded
+constexpr int kVStride = 72;        // V^T row stride in LDS (bf16), padded
+constexpr int kXcds = 8;
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 w) { return __builtin_bit_cast(bf16x8, w); }
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const __bf16 a = (__bf16)lo, b = (__bf16)hi;
+  return (uint32_t)__builtin_bit_cast(uint16_t, a) |
+         ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+}
+
+// Position of key quad m (keys 4m .. 4m+3 of a 64-key sub-block) in the
+// permuted V^T row: within each 16-key group, key 8a + 4h + q sits at 8h + 4a + q.
+__device__ __forceinline__ int vquad_pos(int m) {
+  return 16 * (m >> 2) + 8 * (m & 1) + 4 * ((m >> 1) & 1);
+}
+
+struct KVRegs {
+  uint4 k[4];
+  uint4 v[4];
+};
+
+// Global -> registers for one 64-key sub-block starting at key k0.  Rows at
+// or past N are zero-filled (their scores are masked).
+__device__ __forceinline__ void load_kv(KVRegs& R, const uint16_t* __restrict__ kh,
+                                        const uint16_t* __restrict__ vh, int k0, int N,
+                                        int tid) {
+  const int c = tid & 15;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = k0 + (tid >> 4) + 16 * i;
+    R.k[i] = row < N ? *(const uint4*)(kh + (size_t)row * kHeadDim + 8 * c)
+                     : make_uint4(0, 0, 0, 0);
+  }
+  const int m = tid & 15, cv = tid >> 4;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = k0 + 4 * m + i;
+    R.v[i] = row < N ? *(const uint4*)(vh + (size_t)row * kHeadDim + 8 * cv)
+                     : make_uint4(0, 0, 0, 0);
+  }
+}
+
+__device__ __forceinline__ void store_kv(const KVRegs& R, uint16_t* Ks, uint16_t* Vt, int tid) {
+  const int c = tid & 15;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    *(uint4*)(Ks + ((tid >> 4) + 16 * i) * kKStride + 8 * c) = R.k[i];
+  const int m = tid & 15, cv = tid >> 4;
+  const int pos = vquad_pos(m);
+  const uint32_t w[4][4] = {{R.v[0].x, R.v[0].y, R.v[0].z, R.v[0].w},
+                            {R.v[1].x, R.v[1].y, R.v[1].z, R.v[1].w},
+                            {R.v[2].x, R.v[2].y, R.v[2].z, R.v[2].w},
+                            {R.v[3].x, R.v[3].y, R.v[3].z, R.v[3].w}};
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    // dim 8 cv + e of keys 4m .. 4m+3
+    const int sh = (e & 1) ? 16 : 0;
+    const uint32_t x0 = (w[0][e >> 1] >> sh) & 0xffffu, x1 = (w[1][e >> 1] >> sh) & 0xffffu;
+    const uint32_t x2 = (w[2][e >> 1] >> sh) & 0xffffu, x3 = (w[3][e >> 1] >> sh) & 0xffffu;
+    *(uint2*)(Vt + (8 * cv + e) * kVStride + pos) = make_uint2(x0 | (x1 << 16), x2 | (x3 << 16));
+  }
+}
+
+template <int MODE>
+__global__ __launch_bounds__(kThreads, 2) void attn_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+    const uint16_t* __restrict__ v, uint16_t* __restrict__ o, int B, int Hq, int Hkv, int N,
+    int n_tiles, int Ls, int sub_per_block, int CS, int CB, float sc_log2,
+    const int32_t* __restrict__ bidx, const int32_t* __restrict__ bcnt, int kmax) {
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[kSub * kKStride];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[kHeadDim * kVStride];
+
+  const int G = Hq / Hkv;
+  const int64_t total = (int64_t)B * Hq * n_tiles;
+  const int64_t per_xcd = (int64_t)gridDim.x / kXcds;
+  const int64_t logical = (int64_t)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+  if (logical >= total) return;
+  int64_t t = logical;
+  const int hh = (int)(t % G);
+  t /= G;
+  const int tile = n_tiles - 1 - (int)(t % n_tiles);
+  t /= n_tiles;
+  const int g = (int)(t % Hkv);
+  const int b = (int)(t / Hkv);
+  const int h = g * G + hh;
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int jq = lane & 31, hf = lane >> 5;
+  const int q0 = tile * kTileQ;
+  const int q_last = min(q0 + kTileQ - 1, N - 1);
+  const int qw0 = q0 + wave * 32;          // first query row of this wave
+  const int qrow = qw0 + jq;               // this lane's query row
+
+  const uint16_t* kh = k + (size_t)(b * Hkv + g) * N * kHeadDim;
+  const uint16_t* vh = v + (size_t)(b * Hkv + g) * N * kHeadDim;
+
+  // Q^T fragments (B operand of S^T = K Q^T), kept in registers.
+  bf16x8 qf[8];
+  {
+    const uint16_t* qp = q + ((size_t)(b * Hq + h) * N + qrow) * kHeadDim + 8 * hf;
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+      qf[s] = as_bf16x8(qrow < N ? *(const uint4*)(qp + 16 * s) : make_uint4(0, 0, 0, 0));
+  }
+
+  // The sub-blocks to visit.
+  const int32_t* lst = nullptr;
+  int n_steps;
+  if (MODE == kSparse) {
+    const int seg = q0 / Ls;
+    lst = bidx + ((size_t)(b * Hq + h) * CS + seg) * kmax;
+    const int c = min(max(bcnt[(size_t)(b * Hq + h) * CS + seg], 0), kmax);
+    int nv = 0, prev = -1;
+    while (nv < c) {
+      const int blk = lst[nv];
+      if (blk <= prev || blk >= CB) break;
+      if (blk * sub_per_block * kSub > q_last) break;   // ascending: the rest is in the future
+      prev = blk;
+      ++nv;
+    }
+    n_steps = nv * sub_per_block;
+  } else if (MODE == kDenseCausal) {
+    n_steps = q_last / kSub + 1;
+  } else {
+    n_steps = (N + kSub - 1) / kSub;
+  }
+  auto step_key0 = [&](int i) -> int {
+    if (MODE == kSparse) return (lst[i / sub_per_block] * sub_per_block + i % sub_per_block) * kSub;
+    return i * kSub;
+  };
+
+  f32x16 oacc[4];
+#pragma unroll
+  for (int d = 0; d < 4; ++d)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[d][r] = 0.0f;
+  float m_i = -INFINITY, l_i = 0.0f;
+
+  KVRegs R;
+  if (n_steps > 0) load_kv(R, kh, vh, step_key0(0), N, tid);
+
+  for (int i = 0; i < n_steps; ++i) {
+    const int k0 = step_key0(i);
+    __syncthreads();
+    store_kv(R, Ks, Vt, tid);
+    __syncthreads();
+    if (i + 1 < n_steps) load_kv(R, kh, vh, step_key0(i + 1), N, tid);
+
+    const bool active = (MODE == kDenseFull) || (k0 <= qw0 + 31);
+    if (!active || qw0 >= N) continue;
+
+    // S^T = K Q^T for the 64 keys (two 32-key tiles).
+    f32x16 sacc[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[u][r] = 0.0f;
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        const bf16x8 a = as_bf16x8(*(const uint4*)(Ks + (32 * u + jq) * kKStride + 16 * s + 8 * hf));
+        sacc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[s], sacc[u], 0, 0, 0);
+      }
+    }
+    // scale into base-2 logits, mask future / out-of-range keys
+    const bool need_mask = (MODE != kDenseFull && k0 + kSub - 1 > qw0) || (k0 + kSub > N);
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float sv = sacc[u][r] * sc_log2;
+        if (need_mask) {
+          const int key = k0 + 32 * u + 8 * (r >> 2) + 4 * hf + (r & 3);
+          if (key >= N || (MODE != kDenseFull && key > qrow)) sv = -INFINITY;
+        }
+        sacc[u][r] = sv;
+      }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[u][r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_i, mx);
+    const float m_use = (m_new == -INFINITY) ? 0.0f : m_new;
+    const float alpha = __builtin_amdgcn_exp2f(m_i - m_use);
+    float lsum = 0.0f;
+    uint4 pw[4];   // P^T as bf16, one 16-key MFMA step each
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int u = s >> 1, base = 8 * (s & 1);
+      float p[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        p[e] = __builtin_amdgcn_exp2f(sacc[u][base + e] - m_use);
+        lsum += p[e];
+      }
+      pw[s] = make_uint4(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
+                         pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7]));
+    }
+    l_i = l_i * alpha + lsum;
+    m_i = m_new;
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[d][r] *= alpha;
+    // O^T += V^T P^T
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const bf16x8 a = as_bf16x8(*(const uint4*)(Vt + (32 * d + jq) * kVStride + 16 * s + 8 * hf));
+        oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(pw[s]), oacc[d], 0, 0, 0);
+      }
+    }
+  }
+
+  if (qrow >= N) return;
+  const float l = l_i + __shfl_xor(l_i, 32);
+  const float inv = l > 0.0f ? 1.0f / l : 0.0f;
+  uint16_t* op = o + ((size_t)(b * Hq + h) * N + qrow) * kHeadDim;
+#pragma unroll
+  for (int d = 0; d < 4; ++d)
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      const int dim = 32 * d + 8 * gq + 4 * hf;
+      *(uint2*)(op + dim) =
+          make_uint2(pack_bf16x2(oacc[d][4 * gq] * inv, oacc[d][4 * gq + 1] * inv),
+                     pack_bf16x2(oacc[d][4 * gq + 2] * inv, oacc[d][4 * gq + 3] * inv));
+    }
+}
+
+template <int MODE>
+hipError_t launch_t(const uint16_t* q, const uint16_t* k, const uint16_t* v, const AttnShape& s,
+                    const int32_t* bidx, const int32_t* bcnt, uint16_t* o, hipStream_t stream) {
+  const int n_tiles = (s.N + kTileQ - 1) / kTileQ;
+  const int64_t total = (int64_t)s.B * s.Hq * n_tiles;
+  const int64_t grid = (total + kXcds - 1) / kXcds * kXcds;
+  const float sc_log2 = (float)((double)s.softmax_scale * 1.4426950408889634);
+  hipLaunchKernelGGL(attn_kernel<MODE>, dim3((unsigned)grid), dim3(kThreads), 0, stream, q, k, v,
+                     o, s.B, s.Hq, s.Hkv, s.N, n_tiles, s.Ls, s.Lb / kSub, s.CS, s.CB, sc_log2,
+                     bidx, bcnt, s.kmax);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                            const AttnShape& s, AttnMode mode, const int32_t* block_idx,
+                            const int32_t* block_cnt, uint16_t* o, hipStream_t stream) {
+  switch (mode) {
+    case kSparse: return launch_t<kSparse>(q, k, v, s, block_idx, block_cnt, o, stream);
+    case kDenseCausal: return launch_t<kDenseCausal>(q, k, v, s, nullptr, nullptr, o, stream);
+    default: return launch_t<kDenseFull>(q, k, v, s, nullptr, nullptr, o, stream);
+  }
+}
+
+}  // namespace ei

@@ -1,0 +1,97 @@
+// Internal declarations shared by the HIP translation units of
+// libentropyinfer.so: device helpers and the host-side launchers that the
+// C ABI layer (ei_api.hip) calls after validating its arguments.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ei {
+
+constexpr int kHeadDim = 128;
+constexpr int kWave = 64;
+
+// ----------------------------------------------------------------------------
+// Device helpers
+// ----------------------------------------------------------------------------
+
+// The two bf16 halves of a 32-bit word, widened exactly to fp32.
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+__device__ __forceinline__ float wave_max_f32(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+__device__ __forceinline__ double wave_sum_f64(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    uint32_t t = __shfl_xor(v, o);
+    v = t > v ? t : v;
+  }
+  return v;
+}
+
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    uint32_t t = __shfl_xor(v, o);
+    v = t < v ? t : v;
+  }
+  return v;
+}
+
+__device__ __forceinline__ int popc64(uint64_t m) { return __popcll(m); }
+
+// ----------------------------------------------------------------------------
+// Host launchers (arguments already validated; B, N > 0)
+// ----------------------------------------------------------------------------
+
+struct ProbeShape {
+  int B, Hq, Hkv, N, Ls, Lb, CS, CB, r;
+};
+
+// Workspace layout of the probe: Q representation (binary64) then K
+// representation (bf16 bits), both 256-byte aligned.
+size_t probe_qrep_bytes(const ProbeShape& s);
+size_t probe_krep_bytes(const ProbeShape& s);
+// Largest C_B the scores kernel supports (LDS bound); 0 if none.
+bool probe_supported(const ProbeShape& s);
+
+hipError_t launch_probe(const uint16_t* q, const uint16_t* k, const ProbeShape& s,
+                        double probe_scale, float* log_scores, float* entropy, void* workspace,
+                        hipStream_t stream);
+
+struct SelectShape {
+  int B, Hq, N, Ls, Lb, CS, CB, r, kmax;
+  float e_t;
+  double alpha, delta_t;
+  int Bh, mult;
+};
+
+bool select_supported(const SelectShape& s);
+
+hipError_t launch_select(const float* log_scores, const float* entropy, const SelectShape& s,
+                         uint8_t* rigid, int32_t* budget_blocks, int32_t* block_idx,
+                         int32_t* block_cnt, hipStream_t stream);
+
+struct AttnShape {
+  int B, Hq, Hkv, N, Ls, Lb, CS, CB, kmax;
+  float softmax_scale;
+};
+
+enum AttnMode { kSparse = 0, kDenseCausal = 1, kDenseFull = 2 };
+
+hipError_t launch_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                            const AttnShape& s, AttnMode mode, const int32_t* block_idx,
+                            const int32_t* block_cnt, uint16_t* o, hipStream_t stream);
+
+}  // namespace ei

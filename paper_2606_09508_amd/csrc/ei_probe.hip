@@ -1,0 +1,372 @@
+// Entropy probe: Algorithm 1 (min/max representation vectors), Algorithm 2
+// (observation attention from the four max/min logit products) and the row
+// entropy of Section 4.2, for every (batch, query head, segment).
+//
+// Two kernels:
+//  pool_kernel    streams Q and K once from HBM (the bound of the probe) and
+//                 writes Q_max/Q_min per segment in binary64 (so the scores
+//                 kernel can read them as uniform scalar operands) and
+//                 K_max/K_min per key block in bf16 (exact: pooled values are
+//                 input values).
+//  scores_kernel  one workgroup per (b, KV head, segment, chunk of query
+//                 heads).  Each lane owns one visible key block and forms the
+//                 4 logits of every query head of the chunk in binary64 FMA
+//                 (products of bf16 values are exact, so the logits equal the
+//                 plain definition's); it keeps fp32 offsets from a per-wave
+//                 reference in LDS, then one wave per query head evaluates the
+//                 four softmaxes, A = max((S1+S2)/2, (S3+S4)/2) and
+//                 H = -sum A ln A in log space (fp32 terms, fp64 sums).
+#include "ei_internal.h"
+
+#include <math.h>
+
+namespace ei {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWavesPerBlock = kThreads / kWave;
+
+__global__ __launch_bounds__(kThreads) void pool_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, int B, int Hq, int Hkv,
+    int N, int Ls, int Lb, int CS, int CB, double* __restrict__ qrep,
+    uint16_t* __restrict__ krep) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t item = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+  const int64_t nq = (int64_t)B * Hq * CS, nk = (int64_t)B * Hkv * CB;
+  if (item >= nq + nk) return;
+  const bool is_q = item < nq;
+  const int64_t head = is_q ? item / CS : (item - nq) / CB;
+  const int grp = (int)(is_q ? item % CS : (item - nq) % CB);
+  const int L = is_q ? Ls : Lb;
+  const int64_t row0 = (int64_t)grp * L;
+  const int rows = (int)min((int64_t)L, (int64_t)N - row0);
+  const uint16_t* base = (is_q ? q : k) + ((size_t)head * N + row0) * kHeadDim;
+
+  const int c = lane & 15;   // 16-byte chunk: dims 8c .. 8c+7
+  const int ph = lane >> 4;  // row phase 0..3
+  float mx[8], mn[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) { mx[e] = -INFINITY; mn[e] = INFINITY; }
+
+  int r = ph;
+  for (; r + 12 < rows; r += 16) {
+    uint4 w[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      w[u] = *(const uint4*)(base + (size_t)(r + 4 * u) * kHeadDim + 8 * c);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const uint32_t ww[4] = {w[u].x, w[u].y, w[u].z, w[u].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float lo = bf16_lo(ww[e]), hi = bf16_hi(ww[e]);
+        mx[2 * e] = fmaxf(mx[2 * e], lo);
+        mn[2 * e] = fminf(mn[2 * e], lo);
+        mx[2 * e + 1] = fmaxf(mx[2 * e + 1], hi);
+        mn[2 * e + 1] = fminf(mn[2 * e + 1], hi);
+      }
+    }
+  }
+  for (; r < rows; r += 4) {
+    const uint4 w = *(const uint4*)(base + (size_t)r * kHeadDim + 8 * c);
+    const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float lo = bf16_lo(ww[e]), hi = bf16_hi(ww[e]);
+      mx[2 * e] = fmaxf(mx[2 * e], lo);
+      mn[2 * e] = fminf(mn[2 * e], lo);
+      mx[2 * e + 1] = fmaxf(mx[2 * e + 1], hi);
+      mn[2 * e + 1] = fminf(mn[2 * e + 1], hi);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    mx[e] = fmaxf(mx[e], __shfl_xor(mx[e], 16));
+    mx[e] = fmaxf(mx[e], __shfl_xor(mx[e], 32));
+    mn[e] = fminf(mn[e], __shfl_xor(mn[e], 16));
+    mn[e] = fminf(mn[e], __shfl_xor(mn[e], 32));
+  }
+  if (ph != 0) return;
+  if (is_q) {
+    double* out = qrep + ((size_t)head * CS + grp) * 2 * kHeadDim + 8 * c;
+#pragma unroll
+    for (int e = 0; e < 8; e += 2) {
+      *(double2*)(out + e) = make_double2((double)mx[e], (double)mx[e + 1]);
+      *(double2*)(out + kHeadDim + e) = make_double2((double)mn[e], (double)mn[e + 1]);
+    }
+  } else {
+    uint16_t* out = krep + ((size_t)head * CB + grp) * 2 * kHeadDim + 8 * c;
+    uint32_t px[4], pn[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      px[e] = (__float_as_uint(mx[2 * e]) >> 16) | (__float_as_uint(mx[2 * e + 1]) & 0xffff0000u);
+      pn[e] = (__float_as_uint(mn[2 * e]) >> 16) | (__float_as_uint(mn[2 * e + 1]) & 0xffff0000u);
+    }
+    *(uint4*)out = make_uint4(px[0], px[1], px[2], px[3]);
+    *(uint4*)(out + kHeadDim) = make_uint4(pn[0], pn[1], pn[2], pn[3]);
+  }
+}
+
+__device__ __forceinline__ void widen8(const uint4 w, double* out) {
+  const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    out[2 * e] = (double)bf16_lo(ww[e]);
+    out[2 * e + 1] = (double)bf16_hi(ww[e]);
+  }
+}
+
+// ln((exp(a) + exp(b)) / 2) for a, b <= 0, not both near 0.
+__device__ __forceinline__ float log_pair_avg(float a, float b) {
+  const float hi = fmaxf(a, b), lo = fminf(a, b);
+  return hi + log1pf(expf(lo - hi)) - 0.69314718055994531f;
+}
+
+// HPW query heads per workgroup; rows of the score block: 4 logit products
+// (S1..S4) per head.
+template <int HPW>
+__global__ __launch_bounds__(kThreads) void scores_kernel(
+    const double* __restrict__ qrep, const uint16_t* __restrict__ krep,
+    float* __restrict__ log_scores, float* __restrict__ entropy, int Hq, int Hkv, int CS,
+    int CB, int r, int s_lo, int s_hi, int n_hc, int ldy, double probe_scale) {
+  constexpr int R = 4 * HPW;
+  extern __shared__ float smem[];
+  float* ys = smem;                 // [R][ldy] fp32 offsets x - ref
+  float* refs = smem + R * ldy;     // [R][ldy / 64] per-wave references
+  const int nref = ldy >> 6;
+
+  int64_t id = blockIdx.x;
+  const int ns = s_hi - s_lo;
+  const int s = s_hi - 1 - (int)(id % ns);   // heavier segments first
+  id /= ns;
+  const int hc = (int)(id % n_hc);
+  id /= n_hc;
+  const int g = (int)(id % Hkv);
+  const int b = (int)(id / Hkv);
+  const int G = Hq / Hkv;
+  const int h0 = g * G + hc * HPW;
+  const int nh = min(HPW, G - hc * HPW);
+  const int nvis = min((s + 1) * r, CB);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
+
+  const double* qv[HPW];
+#pragma unroll
+  for (int hh = 0; hh < HPW; ++hh)
+    qv[hh] = qrep + ((size_t)(b * Hq + h0 + min(hh, nh - 1)) * CS + s) * 2 * kHeadDim;
+  const uint16_t* kb = krep + (size_t)(b * Hkv + g) * CB * 2 * kHeadDim;
+
+  // Phase 1: exact logits, one key block per lane.
+  for (int j0 = wave * kWave; j0 < nvis; j0 += kThreads) {
+    const int j = j0 + lane;
+    const bool valid = j < nvis;
+    const uint16_t* kr = kb + (size_t)(valid ? j : nvis - 1) * 2 * kHeadDim;
+    double acc[HPW][4];
+#pragma unroll
+    for (int hh = 0; hh < HPW; ++hh)
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) acc[hh][cc] = 0.0;
+#pragma unroll 2
+    for (int d0 = 0; d0 < kHeadDim; d0 += 8) {
+      double kx[8], kn[8];
+      widen8(*(const uint4*)(kr + d0), kx);
+      widen8(*(const uint4*)(kr + kHeadDim + d0), kn);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+#pragma unroll
+        for (int hh = 0; hh < HPW; ++hh) {
+          const double qa = qv[hh][d0 + e], qb = qv[hh][kHeadDim + d0 + e];
+          acc[hh][0] = fma(qa, kx[e], acc[hh][0]);   // S1: Q_max . K_max
+          acc[hh][1] = fma(qa, kn[e], acc[hh][1]);   // S2: Q_max . K_min
+          acc[hh][2] = fma(qb, kx[e], acc[hh][2]);   // S3: Q_min . K_max
+          acc[hh][3] = fma(qb, kn[e], acc[hh][3]);   // S4: Q_min . K_min
+        }
+      }
+    }
+#pragma unroll
+    for (int hh = 0; hh < HPW; ++hh) {
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) {
+        const int row = hh * 4 + cc;
+        const double x = probe_scale * acc[hh][cc];
+        const float ref = wave_max_f32(valid ? (float)x : -INFINITY);
+        if (valid) ys[row * ldy + j] = (float)(x - (double)ref);
+        if (lane == 0) refs[row * nref + (j0 >> 6)] = ref;
+      }
+    }
+  }
+  __syncthreads();
+
+  // Phase 2: one wave per query head.
+  for (int hh = wave; hh < nh; hh += kWavesPerBlock) {
+    const int h = h0 + hh;
+    const int nch = (nvis + 63) >> 6;
+    float M[4];
+#pragma unroll
+    for (int cc = 0; cc < 4; ++cc) {
+      float m = -INFINITY;
+      for (int c = lane; c < nch; c += kWave) m = fmaxf(m, refs[(hh * 4 + cc) * nref + c]);
+      M[cc] = wave_max_f32(m);
+    }
+    // offsets from the row maximum: diff_c[j] = y + (ref_chunk - M_c)
+    float best[4];
+    int bj[4];
+#pragma unroll
+    for (int cc = 0; cc < 4; ++cc) { best[cc] = -INFINITY; bj[cc] = 0x7fffffff; }
+    for (int j = lane; j < nvis; j += kWave) {
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) {
+        const int row = hh * 4 + cc;
+        const float dv = ys[row * ldy + j] + (refs[row * nref + (j >> 6)] - M[cc]);
+        if (dv > best[cc]) { best[cc] = dv; bj[cc] = j; }
+      }
+    }
+#pragma unroll
+    for (int cc = 0; cc < 4; ++cc) {
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) {
+        const float ob = __shfl_xor(best[cc], o);
+        const int oj = __shfl_xor(bj[cc], o);
+        if (ob > best[cc] || (ob == best[cc] && oj < bj[cc])) { best[cc] = ob; bj[cc] = oj; }
+      }
+    }
+    // rest_c = sum over j != argmax of exp(x_j - x_argmax)
+    double rest[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int j = lane; j < nvis; j += kWave) {
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) {
+        const int row = hh * 4 + cc;
+        const float dv = ys[row * ldy + j] + (refs[row * nref + (j >> 6)] - M[cc]);
+        if (j != bj[cc]) rest[cc] += (double)expf(dv - best[cc]);
+      }
+    }
+    double lse[4], dfc[4];
+#pragma unroll
+    for (int cc = 0; cc < 4; ++cc) {
+      rest[cc] = wave_sum_f64(rest[cc]);
+      lse[cc] = log1p(rest[cc]);
+      dfc[cc] = rest[cc] / (1.0 + rest[cc]);
+    }
+    const float lsef[4] = {(float)lse[0], (float)lse[1], (float)lse[2], (float)lse[3]};
+    float* Lrow = log_scores + ((size_t)(b * Hq + h) * CS + s) * CB;
+    double H = 0.0;
+    for (int j = lane; j < nvis; j += kWave) {
+      float ls[4];
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) {
+        const int row = hh * 4 + cc;
+        const float dv = ys[row * ldy + j] + (refs[row * nref + (j >> 6)] - M[cc]);
+        ls[cc] = (j == bj[cc]) ? -lsef[cc] : (dv - best[cc]) - lsef[cc];
+      }
+      const float l12 = (j == bj[0] && j == bj[1]) ? (float)log1p(-0.5 * (dfc[0] + dfc[1]))
+                                                   : log_pair_avg(ls[0], ls[1]);
+      const float l34 = (j == bj[2] && j == bj[3]) ? (float)log1p(-0.5 * (dfc[2] + dfc[3]))
+                                                   : log_pair_avg(ls[2], ls[3]);
+      const float L = fmaxf(l12, l34);
+      Lrow[j] = L;
+      H -= (double)(expf(L) * L);
+    }
+    H = wave_sum_f64(H);
+    if (lane == 0) entropy[(size_t)(b * Hq + h) * CS + s] = (float)H;
+  }
+}
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+constexpr size_t kMaxLds = 160 * 1024;
+
+size_t scores_lds_bytes(int hpw, int ldy) {
+  const size_t R = 4 * (size_t)hpw;
+  return R * (size_t)ldy * 4 + R * (size_t)(ldy / 64) * 4;
+}
+
+// Heads per workgroup: up to 4 query heads of one KV group share each K
+// representation load; fewer when the LDS tile for this row length would
+// not fit.  0 if even one head does not fit.
+int pick_hpw(int G, int ldy, size_t max_lds) {
+  int hpw = G >= 4 ? 4 : (G >= 2 ? 2 : 1);
+  while (hpw >= 1 && scores_lds_bytes(hpw, ldy) > max_lds) hpw /= 2;
+  return hpw;
+}
+
+size_t device_max_lds() {
+  int dev = 0, v = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return kMaxLds;
+  if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess ||
+      v <= 0)
+    return kMaxLds;
+  return (size_t)v < kMaxLds ? (size_t)v : kMaxLds;
+}
+
+template <int HPW>
+hipError_t launch_scores_t(const double* qrep, const uint16_t* krep, float* log_scores,
+                           float* entropy, const ProbeShape& s, int s_lo, int s_hi, int ldy,
+                           double probe_scale, hipStream_t stream) {
+  const int G = s.Hq / s.Hkv;
+  const int n_hc = (G + HPW - 1) / HPW;
+  const int64_t grid = (int64_t)s.B * s.Hkv * n_hc * (s_hi - s_lo);
+  const size_t lds = scores_lds_bytes(HPW, ldy);
+  hipLaunchKernelGGL(scores_kernel<HPW>, dim3((unsigned)grid), dim3(kThreads), lds, stream, qrep,
+                     krep, log_scores, entropy, s.Hq, s.Hkv, s.CS, s.CB, s.r, s_lo, s_hi, n_hc,
+                     ldy, probe_scale);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t probe_qrep_bytes(const ProbeShape& s) {
+  return align_up((size_t)s.B * s.Hq * s.CS * 2 * kHeadDim * sizeof(double));
+}
+size_t probe_krep_bytes(const ProbeShape& s) {
+  return align_up((size_t)s.B * s.Hkv * s.CB * 2 * kHeadDim * sizeof(uint16_t));
+}
+
+bool probe_supported(const ProbeShape& s) {
+  const int ldy = (s.CB + 63) / 64 * 64;
+  return pick_hpw(s.Hq / s.Hkv, ldy, kMaxLds) > 0;
+}
+
+hipError_t launch_probe(const uint16_t* q, const uint16_t* k, const ProbeShape& s,
+                        double probe_scale, float* log_scores, float* entropy, void* workspace,
+                        hipStream_t stream) {
+  double* qrep = (double*)workspace;
+  uint16_t* krep = (uint16_t*)((char*)workspace + probe_qrep_bytes(s));
+  {
+    const int64_t items = (int64_t)s.B * s.Hq * s.CS + (int64_t)s.B * s.Hkv * s.CB;
+    const int64_t grid = (items + kWavesPerBlock - 1) / kWavesPerBlock;
+    hipLaunchKernelGGL(pool_kernel, dim3((unsigned)grid), dim3(kThreads), 0, stream, q, k, s.B,
+                       s.Hq, s.Hkv, s.N, s.Ls, s.Lb, s.CS, s.CB, qrep, krep);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  // Segments are split into launches by visible-row length so that short
+  // rows do not reserve LDS for the longest one.
+  const int G = s.Hq / s.Hkv;
+  const size_t max_lds = device_max_lds();
+  int s_lo = 0;
+  while (s_lo < s.CS) {
+    const int nvis_lo = min((s_lo + 1) * s.r, s.CB);
+    int cap = 512;
+    while (cap < nvis_lo) cap *= 2;
+    // last segment whose row fits in `cap`
+    int s_hi = min(s.CS, cap / s.r);
+    if (s_hi <= s_lo) s_hi = s_lo + 1;
+    const int nvis_hi = min(s_hi * s.r, s.CB);
+    const int ldy = (nvis_hi + 63) / 64 * 64;
+    const int hpw = pick_hpw(G, ldy, max_lds);
+    hipError_t e = hipErrorInvalidValue;
+    if (hpw == 4)
+      e = launch_scores_t<4>(qrep, krep, log_scores, entropy, s, s_lo, s_hi, ldy, probe_scale,
+                             stream);
+    else if (hpw == 2)
+      e = launch_scores_t<2>(qrep, krep, log_scores, entropy, s, s_lo, s_hi, ldy, probe_scale,
+                             stream);
+    else if (hpw == 1)
+      e = launch_scores_t<1>(qrep, krep, log_scores, entropy, s, s_lo, s_hi, ldy, probe_scale,
+                             stream);
+    if (e != hipSuccess) return e;
+    s_lo = s_hi;
+  }
+  return hipSuccess;
+}
+
+}  // namespace ei

@@ -1,0 +1,216 @@
+// Head classification and budget allocation (Algorithm 3) and per-segment
+// top-k key-block selection (Section 4.2, Appendix A Eq. t_topk).
+//
+//  budget_kernel  one workgroup per (b, query head): the rigid test over all
+//                 segment entropies, the ratios |e_s - e_{s-1}| / e_{s-1} in
+//                 parallel, the clamped budget recurrence (inherently
+//                 sequential, one lane) and k_s = min(floor(B_s / L_B), s r).
+//                 binary64 with FP contraction off, in the order the budget
+//                 recurrence is written, so the result is bit-identical to any
+//                 other IEEE evaluation in that order.
+//  topk_kernel    one wave per (b, h, s) row: the row's past-block scores sit
+//                 in registers as order-preserving 32-bit keys; the k-th
+//                 largest key is found bit by bit with ballot counts, ties at
+//                 the threshold keep the highest block indices, and the chosen
+//                 blocks plus the segment's own blocks are written ascending.
+#include "ei_internal.h"
+
+#include <math.h>
+
+#pragma clang fp contract(off)
+
+namespace ei {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kChunk = 1024;
+
+__global__ __launch_bounds__(kThreads) void budget_kernel(
+    const float* __restrict__ entropy, int CS, int r, int Lb, float e_t, double alpha,
+    double delta_t, int Bh, int mult, uint8_t* __restrict__ rigid_out,
+    int32_t* __restrict__ k_out) {
+  __shared__ double delta[kChunk];
+  __shared__ double Bs[kChunk];
+  const int64_t bh = blockIdx.x;
+  const float* e = entropy + bh * CS;
+  int32_t* ko = k_out + bh * CS;
+  const int tid = threadIdx.x;
+
+  int below = 1;
+  for (int s = tid; s < CS; s += kThreads)
+    if (!(e[s] < e_t)) below = 0;
+  below = __syncthreads_and(below);
+  const double B0 = (double)Bh;
+  const double cap = (double)mult * B0;
+  const double a = alpha * B0;
+  if (tid == 0) rigid_out[bh] = (uint8_t)(below ? 1 : 0);
+  if (below) {
+    const int64_t kb = (int64_t)floor(B0 / (double)Lb);
+    for (int s = tid; s < CS; s += kThreads)
+      ko[s] = (int32_t)min(kb, (int64_t)s * r);
+    return;
+  }
+  double Bprev = B0;   // meaningful in thread 0 only
+  for (int c0 = 0; c0 < CS; c0 += kChunk) {
+    const int n = min(kChunk, CS - c0);
+    for (int i = tid; i < n; i += kThreads) {
+      const int s = c0 + i;
+      if (s == 0) { delta[i] = 0.0; continue; }
+      const double ep = (double)e[s - 1], ec = (double)e[s];
+      const double num = fabs(ec - ep);
+      const double ratio = (num == 0.0 && ep == 0.0) ? 0.0 : num / ep;
+      const double t = ratio - delta_t;
+      delta[i] = a * t;
+    }
+    __syncthreads();
+    if (tid == 0) {
+      for (int i = 0; i < n; ++i) {
+        double Bn;
+        if (c0 + i == 0) {
+          Bn = B0;
+        } else {
+          Bn = Bprev + delta[i];
+          if (!(Bn >= B0)) Bn = B0;
+          if (Bn > cap) Bn = cap;
+        }
+        Bs[i] = Bn;
+        Bprev = Bn;
+      }
+    }
+    __syncthreads();
+    for (int i = tid; i < n; i += kThreads) {
+      const int s = c0 + i;
+      const int64_t kb = (int64_t)floor(Bs[i] / (double)Lb);
+      ko[s] = (int32_t)min(kb, (int64_t)s * r);
+    }
+    __syncthreads();
+  }
+}
+
+// Order-preserving key of a binary32 score, shifted by one so that 0 marks
+// an empty slot: NaN -> 1 (below -inf), -0 == +0, larger float -> larger key.
+__device__ __forceinline__ uint32_t score_key(float v) {
+  if (v != v) return 1u;
+  if (v == 0.0f) v = 0.0f;
+  const uint32_t u = __float_as_uint(v);
+  const uint32_t k = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return k + 1u;   // finite/inf keys are <= 0xff800000, so no wrap
+}
+
+template <int SLOTS>
+__global__ __launch_bounds__(kThreads) void topk_kernel(
+    const float* __restrict__ log_scores, const int32_t* __restrict__ kblocks, int64_t rows,
+    int CS, int CB, int r, int kmax, int32_t* __restrict__ idx, int32_t* __restrict__ cnt) {
+  const int64_t row = (int64_t)blockIdx.x * (kThreads / kWave) + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int s = (int)(row % CS);
+  const int npast = s * r;
+  const int kk = kblocks[row];
+  const float* L = log_scores + row * (int64_t)CB;
+  int32_t* out = idx + row * (int64_t)kmax;
+  const int nsl = (npast + kWave - 1) / kWave;
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  int pos = 0;
+
+  if (kk >= npast) {
+    for (int j = lane; j < npast; j += kWave) out[j] = j;
+    pos = npast;
+  } else if (kk > 0) {
+    uint32_t key[SLOTS];
+    uint32_t kmx = 0, kmn = 0xffffffffu;
+#pragma unroll
+    for (int sl = 0; sl < SLOTS; ++sl) {
+      const int j = sl * kWave + lane;
+      key[sl] = (sl < nsl && j < npast) ? score_key(L[j]) : 0u;
+      if (key[sl]) {
+        kmx = key[sl] > kmx ? key[sl] : kmx;
+        kmn = key[sl] < kmn ? key[sl] : kmn;
+      }
+    }
+    kmx = wave_max_u32(kmx);
+    kmn = wave_min_u32(kmn);
+    // Every valid key shares the high bits where kmx and kmn agree; so does
+    // the k-th largest.  Resolve the remaining bits from the top.
+    uint32_t T;
+    if (kmx == kmn) {
+      T = kmx;
+    } else {
+      const int top = 31 - __clz(kmx ^ kmn);
+      T = kmx & ~((top == 31) ? 0xffffffffu : ((2u << top) - 1u));
+      for (int bit = top; bit >= 0; --bit) {
+        const uint32_t cand = T | (1u << bit);
+        int c = 0;
+#pragma unroll
+        for (int sl = 0; sl < SLOTS; ++sl)
+          if (sl < nsl) c += popc64(__ballot(key[sl] >= cand));
+        if (c >= kk) T = cand;
+      }
+    }
+    int gt = 0;
+#pragma unroll
+    for (int sl = 0; sl < SLOTS; ++sl)
+      if (sl < nsl) gt += popc64(__ballot(key[sl] > T));
+    const int need = kk - gt;   // >= 1 keys equal to T, highest indices first
+    int J = 0;
+    {
+      const int top = 31 - __clz(max(npast - 1, 1));
+      for (int bit = top; bit >= 0; --bit) {
+        const int cand = J | (1 << bit);
+        int c = 0;
+#pragma unroll
+        for (int sl = 0; sl < SLOTS; ++sl)
+          if (sl < nsl) c += popc64(__ballot(key[sl] == T && sl * kWave + lane >= cand));
+        if (c >= need) J = cand;
+      }
+    }
+#pragma unroll
+    for (int sl = 0; sl < SLOTS; ++sl) {
+      if (sl >= nsl) break;
+      const int j = sl * kWave + lane;
+      const bool pick = key[sl] > T || (key[sl] == T && j >= J);
+      const uint64_t m = __ballot(pick);
+      if (pick) out[pos + popc64(m & lt_mask)] = j;
+      pos += popc64(m);
+    }
+  }
+  const int dend = min((s + 1) * r, CB);
+  for (int j = npast + lane; j < dend; j += kWave) out[pos + (j - npast)] = j;
+  pos += dend - npast;
+  for (int t = pos + lane; t < kmax; t += kWave) out[t] = -1;
+  if (lane == 0) cnt[row] = pos;
+}
+
+template <int SLOTS>
+hipError_t launch_topk_t(const float* log_scores, const int32_t* kb, const SelectShape& s,
+                         int32_t* idx, int32_t* cnt, hipStream_t stream) {
+  const int64_t rows = (int64_t)s.B * s.Hq * s.CS;
+  const int64_t grid = (rows + (kThreads / kWave) - 1) / (kThreads / kWave);
+  hipLaunchKernelGGL(topk_kernel<SLOTS>, dim3((unsigned)grid), dim3(kThreads), 0, stream,
+                     log_scores, kb, rows, s.CS, s.CB, s.r, s.kmax, idx, cnt);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool select_supported(const SelectShape& s) { return s.CB <= 128 * kWave; }
+
+hipError_t launch_select(const float* log_scores, const float* entropy, const SelectShape& s,
+                         uint8_t* rigid, int32_t* budget_blocks, int32_t* block_idx,
+                         int32_t* block_cnt, hipStream_t stream) {
+  hipLaunchKernelGGL(budget_kernel, dim3((unsigned)(s.B * s.Hq)), dim3(kThreads), 0, stream,
+                     entropy, s.CS, s.r, s.Lb, s.e_t, s.alpha, s.delta_t, s.Bh, s.mult, rigid,
+                     budget_blocks);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int npast_max = (s.CS - 1) * s.r;
+  if (npast_max <= 8 * kWave)
+    return launch_topk_t<8>(log_scores, budget_blocks, s, block_idx, block_cnt, stream);
+  if (npast_max <= 32 * kWave)
+    return launch_topk_t<32>(log_scores, budget_blocks, s, block_idx, block_cnt, stream);
+  if (npast_max <= 64 * kWave)
+    return launch_topk_t<64>(log_scores, budget_blocks, s, block_idx, block_cnt, stream);
+  return launch_topk_t<128>(log_scores, budget_blocks, s, block_idx, block_cnt, stream);
+}
+
+}  // namespace ei

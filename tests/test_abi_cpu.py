@@ -1,0 +1,116 @@
+"""The C ABI without a GPU: the library loads, exports every symbol the header
+declares, its pure helpers return the documented values, and invalid
+arguments are rejected on the host before anything is launched."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_09508_amd import binding as eb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "entropyinfer.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ei_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(eb.LIB_PATH):
+        pytest.skip("libentropyinfer.so is not built")
+    return eb.lib()
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert {"ei_entropy_probe", "ei_select_blocks", "ei_sparse_prefill_attn",
+            "ei_dense_prefill_attn"} <= set(names)
+    for n in names:
+        assert hasattr(L, n), f"{n} declared in the header but not exported"
+
+
+def test_helpers(L):
+    assert L.ei_abi_version() == 1
+    assert eb.kmax(128, 64, 2048, 3) == 98
+    assert eb.kmax(2048, 64, 2048, 3) == 96 + 32
+    assert eb.kmax(256, 128, 256, 3) == 6 + 2
+    d = eb.Dims(1, 32, 8, 131072, 128)
+    assert L.ei_num_segments(d, eb.Tiling(128, 64)) == 1024
+    assert L.ei_num_blocks(d, eb.Tiling(128, 64)) == 2048
+    assert L.ei_num_segments(eb.Dims(1, 4, 1, 1000, 128), eb.Tiling(128, 64)) == 8
+    assert L.ei_num_blocks(eb.Dims(1, 4, 1, 1000, 128), eb.Tiling(128, 64)) == 16
+    ws = L.ei_probe_workspace_bytes(d, eb.Tiling(128, 64))
+    assert ws >= 32 * 1024 * 2 * 128 * 8 + 8 * 2048 * 2 * 128 * 2
+    assert L.ei_probe_workspace_bytes(eb.Dims(1, 4, 1, 1024, 64), eb.Tiling(128, 64)) == 0
+    for st in (0, -1, -2, -3, -4, -5):
+        assert L.ei_status_str(st).decode().startswith(eb._STATUS[st])
+
+
+FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: every call below fails validation
+
+
+@pytest.mark.parametrize("dims,tiling,expect", [
+    (eb.Dims(1, 4, 1, 1024, 64), eb.Tiling(128, 64), -3),     # D != 128
+    (eb.Dims(1, 6, 4, 1024, 128), eb.Tiling(128, 64), -2),    # Hq % Hkv
+    (eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(128, 32), -3),    # L_B not 64/128
+    (eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(192, 64), -3),    # L_S not a multiple of 128
+    (eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(128, 256), -3),
+    (eb.Dims(-1, 4, 1, 1024, 128), eb.Tiling(128, 64), -2),
+    (eb.Dims(1, 0, 1, 1024, 128), eb.Tiling(128, 64), -2),
+])
+def test_probe_rejects_bad_shapes(L, dims, tiling, expect):
+    st = L.ei_entropy_probe(FAKE, FAKE, dims, tiling, 1.0, FAKE, FAKE, FAKE, 1 << 30, None)
+    assert st == expect
+
+
+def test_probe_null_and_workspace(L):
+    d, t = eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(128, 64)
+    assert L.ei_entropy_probe(None, FAKE, d, t, 1.0, FAKE, FAKE, FAKE, 1 << 30, None) == -1
+    assert L.ei_entropy_probe(FAKE, FAKE, d, t, 1.0, None, FAKE, FAKE, 1 << 30, None) == -1
+    need = L.ei_probe_workspace_bytes(d, t)
+    assert L.ei_entropy_probe(FAKE, FAKE, d, t, 1.0, FAKE, FAKE, FAKE, need - 1, None) == -4
+    assert L.ei_entropy_probe(FAKE, FAKE, d, t, 1.0, FAKE, FAKE, None, need, None) == -4
+    assert L.ei_entropy_probe(FAKE, FAKE, d, t, float("nan"), FAKE, FAKE, FAKE, need, None) == -2
+
+
+def test_empty_problems_launch_nothing(L):
+    t = eb.Tiling(128, 64)
+    for d in (eb.Dims(0, 4, 1, 1024, 128), eb.Dims(1, 4, 1, 0, 128)):
+        assert L.ei_entropy_probe(None, None, d, t, 1.0, None, None, None, 0, None) == 0
+        assert L.ei_select_blocks(None, None, d, t, eb.budget_params(), 98, None, None, None,
+                                  None, None) == 0
+        assert L.ei_sparse_prefill_attn(None, None, None, d, t, 0.088, None, None, 98, None,
+                                        None) == 0
+        assert L.ei_dense_prefill_attn(None, None, None, d, 0.088, 1, None, None) == 0
+
+
+def test_select_rejects_bad_params(L):
+    d, t = eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(128, 64)
+    p = eb.budget_params(base_budget=256)
+    km = L.ei_kmax(t, p)
+    args = (FAKE,) * 5
+    assert L.ei_select_blocks(FAKE, FAKE, d, t, p, km - 1, *args) == -2
+    assert L.ei_select_blocks(FAKE, FAKE, d, t, eb.budget_params(base_budget=-1), km, *args) == -2
+    assert L.ei_select_blocks(FAKE, FAKE, d, t, eb.budget_params(mult=0), km, *args) == -2
+    assert L.ei_select_blocks(FAKE, FAKE, d, t, eb.budget_params(alpha=float("nan")), km,
+                              *args) == -2
+    assert L.ei_select_blocks(FAKE, None, d, t, p, km, *args) == -1
+    assert L.ei_select_blocks(FAKE, FAKE, d, t, p, km, FAKE, FAKE, None, FAKE, None) == -1
+
+
+def test_attention_rejects_bad_arguments(L):
+    d, t = eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(128, 64)
+    assert L.ei_sparse_prefill_attn(FAKE, FAKE, FAKE, d, t, 0.088, FAKE, FAKE, 0, FAKE, None) == -2
+    assert L.ei_sparse_prefill_attn(FAKE, FAKE, FAKE, d, t, 0.088, None, FAKE, 10, FAKE,
+                                    None) == -1
+    assert L.ei_sparse_prefill_attn(FAKE, FAKE, FAKE, eb.Dims(1, 4, 1, 1024, 96), t, 0.088, FAKE,
+                                    FAKE, 10, FAKE, None) == -3
+    assert L.ei_dense_prefill_attn(FAKE, FAKE, None, d, 0.088, 1, FAKE, None) == -1
+    assert L.ei_dense_prefill_attn(FAKE, FAKE, FAKE, eb.Dims(1, 5, 2, 64, 128), 0.088, 1, FAKE,
+                                   None) == -2
+    assert L.ei_dense_prefill_attn(FAKE, FAKE, FAKE, d, float("nan"), 1, FAKE, None) == -2

@@ -1,0 +1,269 @@
+"""HIP path vs the CPU oracle, element by element, through the C ABI.
+
+Bars: entropy |dH| <= 1e-4 H + 1e-20; ln A_obs |dL| <= 1e-3 (+1e-6 |L|);
+selection (rigid flags, budgets, block lists, counts) bit-exact given the
+GPU's own fp32 scores; attention max-abs <= 2e-2 against fp64.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_09508_amd import binding as eb
+from paper_2606_09508_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+H_REL, H_ABS = 1e-4, 1e-20
+L_ABS = 1e-3
+ATTN_ABS = 2e-2
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    eb.lib()
+    return torch.device("cuda:0")
+
+
+def to_dev(a: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def bf16_to_f64(t: torch.Tensor) -> np.ndarray:
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def run_path(w, base_budget=None):
+    q, k, v = to_dev(w.q), to_dev(w.k), to_dev(w.v)
+    bh = w.base_budget if base_budget is None else base_budget
+    ls, en = eb.entropy_probe(q, k, w.Ls, w.Lb, w.probe_scale)
+    sel = eb.select_blocks(ls, en, w.N, w.Ls, w.Lb, w.e_t, w.alpha, w.delta_t, bh, w.mult,
+                           n_kv_heads=w.Hkv)
+    o = eb.sparse_prefill_attn(q, k, v, sel["idx"], sel["cnt"], w.Ls, w.Lb, w.softmax_scale)
+    torch.cuda.synchronize()
+    return {"q": q, "k": k, "v": v, "ls": ls.cpu().numpy(), "en": en.cpu().numpy(),
+            "sel": {kk: t.cpu().numpy() for kk, t in sel.items()}, "o": o, "bh": bh}
+
+
+def check_probe(w, r, rows=None):
+    """rows: optional [n, 3] (b, h, s) sample; default every row."""
+    if rows is None:
+        Lr, Hr = oracle.probe(w.q, w.k, w.Ls, w.Lb, w.probe_scale)
+        Lr = Lr.reshape(-1, w.CB)
+        Hr = Hr.reshape(-1)
+        Lg = r["ls"].reshape(-1, w.CB)
+        Hg = r["en"].reshape(-1)
+        sidx = np.tile(np.arange(w.CS), w.B * w.Hq)
+    else:
+        Lr, Hr = oracle.probe(w.q, w.k, w.Ls, w.Lb, w.probe_scale, rows=rows)
+        Lg = np.stack([r["ls"][b, h, s] for b, h, s in rows])
+        Hg = np.array([r["en"][b, h, s] for b, h, s in rows])
+        sidx = rows[:, 2]
+    herr = np.abs(Hg.astype(np.float64) - Hr)
+    assert (herr <= H_REL * Hr + H_ABS).all(), \
+        f"entropy: worst rel {np.max(herr / np.maximum(Hr, 1e-300)):.3e}"
+    r_ = w.Ls // w.Lb
+    worst = 0.0
+    for t in range(len(Hr)):
+        nv = min((int(sidx[t]) + 1) * r_, w.CB)
+        d = np.abs(Lg[t, :nv].astype(np.float64) - Lr[t, :nv])
+        assert (d <= L_ABS + 1e-6 * np.abs(Lr[t, :nv])).all(), f"log_scores row {t}: {d.max()}"
+        worst = max(worst, float(d.max()))
+    return float(np.max(herr / np.maximum(Hr, 1e-30))), worst
+
+
+def check_select(w, r):
+    ref = oracle.select(r["ls"], r["en"], w.N, w.Ls, w.Lb, w.e_t, w.alpha, w.delta_t, r["bh"],
+                        w.mult)
+    g = r["sel"]
+    np.testing.assert_array_equal(g["rigid"], ref["rigid"])
+    np.testing.assert_array_equal(g["budget"], ref["budget"])
+    np.testing.assert_array_equal(g["cnt"], ref["cnt"])
+    np.testing.assert_array_equal(g["idx"], ref["idx"])
+
+
+def check_attention(w, r, rows=None):
+    if rows is None:
+        rows = np.array([[b, h, i] for b in range(w.B) for h in range(w.Hq) for i in range(w.N)],
+                        np.int32)
+    ref = oracle.attention(w.q, w.k, w.v, rows, w.softmax_scale, True, r["sel"]["idx"],
+                           r["sel"]["cnt"], w.Ls, w.Lb)
+    o = bf16_to_f64(r["o"])
+    got = o[rows[:, 0], rows[:, 1], rows[:, 2]]
+    err = np.abs(got - ref)
+    assert err.max() <= ATTN_ABS, f"sparse attention max-abs {err.max():.3e}"
+    return float(err.max()), float(err.mean())
+
+
+C1_CASES = [
+    dict(),                                           # the tiny workload itself
+    dict(N=1000),                                     # ragged tail
+    dict(N=1088),
+    dict(N=128),                                      # a single segment
+    dict(N=64),                                       # shorter than one segment
+    dict(B=2, N=640),
+    dict(Hq=4, Hkv=4),                                # MHA
+    dict(Hq=7, Hkv=1, N=512),                         # G = 7
+    dict(Hq=8, Hkv=2, N=768),
+    dict(Ls=256, Lb=64, N=1280),
+    dict(Ls=256, Lb=128, N=1280, base_budget=512),
+    dict(Ls=2048, Lb=64, N=4096, base_budget=1024),
+    dict(N=2048, base_budget=64),                     # k = 1 past block
+    dict(N=2048, base_budget=0),                      # own blocks only
+]
+
+
+@pytest.mark.parametrize("case", C1_CASES, ids=lambda c: ",".join(f"{k}={v}" for k, v in c.items())
+                         or "c1")
+@pytest.mark.parametrize("seed", [0, 1])
+def test_path_parity_small(case, seed):
+    w = synth.make("c1", seed, **case)
+    say(f"[small] seed={seed} {case}")
+    r = run_path(w)
+    hrel, lerr = check_probe(w, r)
+    check_select(w, r)
+    amax, amean = check_attention(w, r)
+    say(f"  entropy rel {hrel:.2e}  logscore abs {lerr:.2e}  attn max {amax:.2e} mean {amean:.2e}")
+
+
+def test_c1_labels_on_gpu():
+    """The tiny workload's intended head types come out of the GPU path."""
+    w = synth.make("c1", 0)
+    r = run_path(w)
+    assert list(r["sel"]["rigid"][0]) == [1, 1, 0, 0]
+
+
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("case", [dict(), dict(N=1000), dict(B=2, Hq=8, Hkv=2, N=384),
+                                  dict(N=64)])
+def test_dense_parity(case, causal):
+    w = synth.make("c1", 7, **case)
+    say(f"[dense] causal={causal} {case}")
+    q, k, v = to_dev(w.q), to_dev(w.k), to_dev(w.v)
+    o = eb.dense_prefill_attn(q, k, v, w.softmax_scale, causal)
+    torch.cuda.synchronize()
+    rows = np.array([[b, h, i] for b in range(w.B) for h in range(w.Hq) for i in range(w.N)],
+                    np.int32)
+    ref = oracle.attention(w.q, w.k, w.v, rows, w.softmax_scale, causal)
+    got = bf16_to_f64(o)[rows[:, 0], rows[:, 1], rows[:, 2]]
+    assert np.abs(got - ref).max() <= ATTN_ABS
+
+
+def test_full_budget_sparse_is_dense_bitwise():
+    """With B_h >= N every visible block is selected; the sparse kernel then
+    visits exactly the dense kernel's blocks in the same order."""
+    w = synth.make("c1", 2, N=1280)
+    r = run_path(w, base_budget=w.N)
+    assert (r["sel"]["cnt"] == 2 * (np.arange(w.CS) + 1)[None, None, :]).all()
+    od = eb.dense_prefill_attn(r["q"], r["k"], r["v"], w.softmax_scale, True)
+    torch.cuda.synchronize()
+    assert torch.equal(od, r["o"])
+
+
+def test_deterministic():
+    w = synth.make("c2", 3, N=4096)
+    a = run_path(w)
+    b = run_path(w)
+    assert np.array_equal(a["en"], b["en"])
+    assert np.array_equal(a["ls"][~np.isnan(a["ls"])], b["ls"][~np.isnan(a["ls"])])
+    assert np.array_equal(a["sel"]["idx"], b["sel"]["idx"])
+    assert torch.equal(a["o"], b["o"])
+
+
+def test_malformed_block_list_is_safe():
+    """Out-of-range, descending and oversized counts stop the list walk."""
+    w = synth.make("c1", 4, N=512)
+    q, k, v = to_dev(w.q), to_dev(w.k), to_dev(w.v)
+    km = w.kmax
+    idx = torch.full((1, w.Hq, w.CS, km), -1, dtype=torch.int32)
+    cnt = torch.zeros((1, w.Hq, w.CS), dtype=torch.int32)
+    for s in range(w.CS):
+        own = [2 * s, 2 * s + 1]
+        idx[0, 0, s, :2] = torch.tensor(own)
+        cnt[0, 0, s] = 2
+        idx[0, 1, s, :3] = torch.tensor([10 ** 6] + own)         # out of range first
+        cnt[0, 1, s] = 3
+        idx[0, 2, s, :2] = torch.tensor(own)
+        cnt[0, 2, s] = 10 ** 6                                    # count beyond kmax
+        idx[0, 3, s, :3] = torch.tensor(own + [0])               # not ascending
+        cnt[0, 3, s] = 3
+    o = eb.sparse_prefill_attn(q, k, v, idx.cuda(), cnt.cuda(), w.Ls, w.Lb, w.softmax_scale)
+    torch.cuda.synchronize()
+    of = o.float().cpu()
+    assert torch.isfinite(of).all()
+    assert (of[0, 1] == 0).all()                                  # nothing visible -> zeros
+    rows = np.array([[0, h, i] for h in (0, 2, 3) for i in range(w.N)], np.int32)
+    ref_idx = idx.numpy().copy()
+    ref_cnt = np.full((1, w.Hq, w.CS), 2, np.int32)
+    ref = oracle.attention(w.q, w.k, w.v, rows, w.softmax_scale, True, ref_idx, ref_cnt, w.Ls,
+                           w.Lb)
+    got = of.numpy().astype(np.float64)[rows[:, 0], rows[:, 1], rows[:, 2]]
+    assert np.abs(got - ref).max() <= ATTN_ABS
+
+
+def _sample_rows(w, n_seg=48, seed=0):
+    rng = np.random.default_rng(seed)
+    segs = np.unique(np.concatenate([[0, 1, w.CS - 1], rng.integers(0, w.CS, n_seg)]))
+    rows = []
+    for s in segs:
+        for h in rng.choice(w.Hq, size=min(3, w.Hq), replace=False):
+            rows.append([0, int(h), int(s)])
+    return np.array(rows, np.int32)
+
+
+def _sample_query_rows(w, n=96, seed=1):
+    rng = np.random.default_rng(seed)
+    idx = set()
+    for i in list(rng.integers(0, w.N, n)) + [0, 1, w.Ls - 1, w.Ls, w.N - 1, w.N - 2]:
+        idx.add(int(i))
+    heads = rng.integers(0, w.Hq, len(idx))
+    return np.array([[0, int(h), i] for h, i in zip(heads, sorted(idx))], np.int32)
+
+
+def test_c2_llama8b_32k():
+    w = synth.make("c2", 0)
+    say("[c2] generated")
+    r = run_path(w)
+    hrel, lerr = check_probe(w, r)
+    check_select(w, r)
+    amax, amean = check_attention(w, r, _sample_query_rows(w))
+    frac = float((r["en"] < w.e_t).mean())
+    say(f"  entropy rel {hrel:.2e} L {lerr:.2e} attn {amax:.2e}/{amean:.2e} rigid-seg {frac:.3f}")
+    assert 0.3 < frac < 0.5
+
+
+@pytest.fixture(scope="module")
+def c3():
+    w = synth.make("c3", 0)
+    say("[c3] generated")
+    return w, run_path(w)
+
+
+def test_c3_llama8b_128k_sampled(c3):
+    """Bench workload, same launch configuration: sampled probe rows and query
+    rows, full selection."""
+    w, r = c3
+    hrel, lerr = check_probe(w, r, _sample_rows(w))
+    say(f"  probe ok: entropy rel {hrel:.2e}, L {lerr:.2e}")
+    check_select(w, r)
+    say("  select bit-exact")
+    amax, amean = check_attention(w, r, _sample_query_rows(w, n=48))
+    say(f"  attn max {amax:.2e} mean {amean:.2e}")
+
+
+def test_c3_dense_sampled(c3):
+    w, r = c3
+    od = eb.dense_prefill_attn(r["q"], r["k"], r["v"], w.softmax_scale, True)
+    torch.cuda.synchronize()
+    rows = _sample_query_rows(w, n=24, seed=5)
+    ref = oracle.attention(w.q, w.k, w.v, rows, w.softmax_scale, True)
+    got = bf16_to_f64(od)[rows[:, 0], rows[:, 1], rows[:, 2]]
+    assert np.abs(got - ref).max() <= ATTN_ABS
