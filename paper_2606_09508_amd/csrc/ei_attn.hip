@@ -21,10 +21,14 @@
 // stored in LDS with the matching key permutation so that P^T can be fed to
 // the second product straight from registers.
 //
-// Workgroups are mapped so that each XCD (dispatched round-robin) receives a
-// contiguous run of (batch, KV head, tile, query head) work: the G query
-// heads that share a K/V head, and neighbouring tiles, run on one XCD and
-// reuse K/V blocks from its L2.  Heavier (later) tiles are issued first.
+// Dense workgroups are mapped so that each XCD (dispatched round-robin)
+// receives a contiguous run of (batch, KV head, tile, query head) work: the G
+// query heads that share a K/V head, and neighbouring tiles, run on one XCD
+// and reuse K/V blocks from its L2.  Sparse work per head is uneven (budgets
+// differ per head, up to 3x), so a fixed head -> XCD assignment leaves the
+// XCD with the heaviest heads finishing last; instead the KV groups rotate
+// over the XCDs from one tile to the next.  Heavier (later) tiles are issued
+// first in both.
 #include "ei_internal.h"
 
 #include <math.h>
@@ -34,6 +38,8 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kThreads = 256;
 constexpr int kTileQ = 128;
@@ -44,10 +50,10 @@ constexpr int kXcds = 8;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 w) { return __builtin_bit_cast(bf16x8, w); }
 
+// Two fp32 values -> packed bf16 pair (round to nearest even), one instruction.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  const __bf16 a = (__bf16)lo, b = (__bf16)hi;
-  return (uint32_t)__builtin_bit_cast(uint16_t, a) |
-         ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+  const f32x2 x = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(x, bf16x2));
 }
 
 // Position of key quad m (keys 4m .. 4m+3 of a 64-key sub-block) in the
@@ -66,65 +72,109 @@ struct KVRegs {
 __device__ __forceinline__ void load_kv(KVRegs& R, const uint16_t* __restrict__ kh,
                                         const uint16_t* __restrict__ vh, int k0, int N,
                                         int tid) {
-  const int c = tid & 15;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = k0 + (tid >> 4) + 16 * i;
-    R.k[i] = row < N ? *(const uint4*)(kh + (size_t)row * kHeadDim + 8 * c)
-                     : make_uint4(0, 0, 0, 0);
-  }
+  const int c = tid & 15, r0 = tid >> 4;
   const int m = tid & 15, cv = tid >> 4;
+  if (k0 + kSub <= N) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = k0 + 4 * m + i;
-    R.v[i] = row < N ? *(const uint4*)(vh + (size_t)row * kHeadDim + 8 * cv)
-                     : make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < 4; ++i)
+      R.k[i] = *(const uint4*)(kh + (size_t)(k0 + r0 + 16 * i) * kHeadDim + 8 * c);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      R.v[i] = *(const uint4*)(vh + (size_t)(k0 + 4 * m + i) * kHeadDim + 8 * cv);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = k0 + r0 + 16 * i;
+      R.k[i] = row < N ? *(const uint4*)(kh + (size_t)row * kHeadDim + 8 * c)
+                       : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = k0 + 4 * m + i;
+      R.v[i] = row < N ? *(const uint4*)(vh + (size_t)row * kHeadDim + 8 * cv)
+                       : make_uint4(0, 0, 0, 0);
+    }
   }
 }
 
+// Registers -> LDS: K row-major; V transposed (head dim major) with the key
+// permutation above, packing each dim of a key quad with two byte permutes.
 __device__ __forceinline__ void store_kv(const KVRegs& R, uint16_t* Ks, uint16_t* Vt, int tid) {
   const int c = tid & 15;
 #pragma unroll
   for (int i = 0; i < 4; ++i)
     *(uint4*)(Ks + ((tid >> 4) + 16 * i) * kKStride + 8 * c) = R.k[i];
   const int m = tid & 15, cv = tid >> 4;
-  const int pos = vquad_pos(m);
-  const uint32_t w[4][4] = {{R.v[0].x, R.v[0].y, R.v[0].z, R.v[0].w},
-                            {R.v[1].x, R.v[1].y, R.v[1].z, R.v[1].w},
-                            {R.v[2].x, R.v[2].y, R.v[2].z, R.v[2].w},
-                            {R.v[3].x, R.v[3].y, R.v[3].z, R.v[3].w}};
+  uint16_t* vb = Vt + (8 * cv) * kVStride + vquad_pos(m);
+  const uint32_t w0[4] = {R.v[0].x, R.v[0].y, R.v[0].z, R.v[0].w};
+  const uint32_t w1[4] = {R.v[1].x, R.v[1].y, R.v[1].z, R.v[1].w};
+  const uint32_t w2[4] = {R.v[2].x, R.v[2].y, R.v[2].z, R.v[2].w};
+  const uint32_t w3[4] = {R.v[3].x, R.v[3].y, R.v[3].z, R.v[3].w};
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    // dim 8 cv + e of keys 4m .. 4m+3
-    const int sh = (e & 1) ? 16 : 0;
-    const uint32_t x0 = (w[0][e >> 1] >> sh) & 0xffffu, x1 = (w[1][e >> 1] >> sh) & 0xffffu;
-    const uint32_t x2 = (w[2][e >> 1] >> sh) & 0xffffu, x3 = (w[3][e >> 1] >> sh) & 0xffffu;
-    *(uint2*)(Vt + (8 * cv + e) * kVStride + pos) = make_uint2(x0 | (x1 << 16), x2 | (x3 << 16));
+  for (int qd = 0; qd < 4; ++qd) {
+    // dims 8 cv + 2 qd (low halves) and 8 cv + 2 qd + 1 (high halves)
+    const uint32_t lo01 = __builtin_amdgcn_perm(w1[qd], w0[qd], 0x05040100u);
+    const uint32_t lo23 = __builtin_amdgcn_perm(w3[qd], w2[qd], 0x05040100u);
+    const uint32_t hi01 = __builtin_amdgcn_perm(w1[qd], w0[qd], 0x07060302u);
+    const uint32_t hi23 = __builtin_amdgcn_perm(w3[qd], w2[qd], 0x07060302u);
+    *(uint2*)(vb + (2 * qd) * kVStride) = make_uint2(lo01, lo23);
+    *(uint2*)(vb + (2 * qd + 1) * kVStride) = make_uint2(hi01, hi23);
   }
 }
 
-template <int MODE>
+// Lazy rescaling: the running maximum is only raised when a new score exceeds
+// it by more than 2^8 (base-2 units), so exp2 arguments stay <= 8 and O, l are
+// rescaled rarely; O and l always share the same reference, so the result is
+// the exact softmax.
+constexpr float kRescaleThreshold = 8.0f;
+
+template <int MODE, int SUB>
 __global__ __launch_bounds__(kThreads, 2) void attn_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ v, uint16_t* __restrict__ o, int B, int Hq, int Hkv, int N,
-    int n_tiles, int Ls, int sub_per_block, int CS, int CB, float sc_log2,
-    const int32_t* __restrict__ bidx, const int32_t* __restrict__ bcnt, int kmax) {
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[kSub * kKStride];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[kHeadDim * kVStride];
+    int n_tiles, int Ls, int CS, int CB, float sc_log2, const int32_t* __restrict__ bidx,
+    const int32_t* __restrict__ bcnt, int kmax) {
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kSub * kKStride];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][kHeadDim * kVStride];
 
-  const int G = Hq / Hkv;
-  const int64_t total = (int64_t)B * Hq * n_tiles;
-  const int64_t per_xcd = (int64_t)gridDim.x / kXcds;
-  const int64_t logical = (int64_t)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
-  if (logical >= total) return;
-  int64_t t = logical;
-  const int hh = (int)(t % G);
-  t /= G;
-  const int tile = n_tiles - 1 - (int)(t % n_tiles);
-  t /= n_tiles;
-  const int g = (int)(t % Hkv);
-  const int b = (int)(t / Hkv);
-  const int h = g * G + hh;
+  const unsigned G = (unsigned)(Hq / Hkv);
+  const unsigned total = (unsigned)B * (unsigned)Hq * (unsigned)n_tiles;
+  int hh, tile, g, b;
+  if (MODE != kSparse) {
+    const unsigned per_xcd = gridDim.x / kXcds;
+    unsigned t = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+    if (t >= total) return;
+    hh = (int)(t % G);
+    t /= G;
+    tile = n_tiles - 1 - (int)(t % (unsigned)n_tiles);
+    t /= (unsigned)n_tiles;
+    g = (int)(t % (unsigned)Hkv);
+    b = (int)(t / (unsigned)Hkv);
+  } else if (((unsigned)B * (unsigned)Hkv) % kXcds == 0) {
+    // Tile-major, heavier tiles first; at tile t, XCD x takes the KV groups
+    // bg with (bg + t) % 8 == x (all G query heads of each), so a group's
+    // work rotates over every XCD.
+    if (blockIdx.x >= total) return;
+    const unsigned x = blockIdx.x % kXcds, idx = blockIdx.x / kXcds;
+    const unsigned per_tile = ((unsigned)B * (unsigned)Hq) / kXcds;
+    const unsigned tr = idx / per_tile, rem = idx % per_tile;
+    tile = n_tiles - 1 - (int)tr;
+    hh = (int)(rem % G);
+    const unsigned bg = (x + kXcds - (unsigned)tile % kXcds) % kXcds + kXcds * (rem / G);
+    b = (int)(bg / (unsigned)Hkv);
+    g = (int)(bg % (unsigned)Hkv);
+  } else {
+    // Tile-major with the (batch, head) index rotated by one per tile.
+    if (blockIdx.x >= total) return;
+    const unsigned R = (unsigned)B * (unsigned)Hq;
+    const unsigned tr = blockIdx.x / R;
+    const unsigned r = (blockIdx.x % R + tr) % R;
+    tile = n_tiles - 1 - (int)tr;
+    b = (int)(r / (unsigned)Hq);
+    hh = (int)(r % (unsigned)Hq) % (int)G;
+    g = (int)(r % (unsigned)Hq) / (int)G;
+  }
+  const int h = g * (int)G + hh;
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -153,22 +203,33 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(
     const int seg = q0 / Ls;
     lst = bidx + ((size_t)(b * Hq + h) * CS + seg) * kmax;
     const int c = min(max(bcnt[(size_t)(b * Hq + h) * CS + seg], 0), kmax);
-    int nv = 0, prev = -1;
-    while (nv < c) {
-      const int blk = lst[nv];
-      if (blk <= prev || blk >= CB) break;
-      if (blk * sub_per_block * kSub > q_last) break;   // ascending: the rest is in the future
-      prev = blk;
-      ++nv;
+    // Valid prefix of the list, 64 entries at a time: strictly ascending,
+    // inside [0, C_B), and not wholly after the tile's last query.
+    int nv = 0;
+    for (int base = 0; base < c; base += kWave) {
+      const int e = base + lane;
+      bool ok = false;
+      if (e < c) {
+        const int blk = lst[e];
+        const int prv = e > 0 ? lst[e - 1] : -1;
+        ok = blk > prv && blk < CB && blk * SUB * kSub <= q_last;
+      }
+      const uint64_t bad = ~__builtin_amdgcn_ballot_w64(ok);
+      if (bad != 0) {
+        nv = base + (int)__builtin_ctzll(bad);
+        break;
+      }
+      nv = base + kWave;
     }
-    n_steps = nv * sub_per_block;
+    nv = min(nv, c);
+    n_steps = nv * SUB;
   } else if (MODE == kDenseCausal) {
     n_steps = q_last / kSub + 1;
   } else {
     n_steps = (N + kSub - 1) / kSub;
   }
   auto step_key0 = [&](int i) -> int {
-    if (MODE == kSparse) return (lst[i / sub_per_block] * sub_per_block + i % sub_per_block) * kSub;
+    if (MODE == kSparse) return (SUB == 1 ? lst[i] : lst[i >> 1] * SUB + (i & 1)) * kSub;
     return i * kSub;
   };
 
@@ -180,81 +241,90 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(
   float m_i = -INFINITY, l_i = 0.0f;
 
   KVRegs R;
-  if (n_steps > 0) load_kv(R, kh, vh, step_key0(0), N, tid);
+  if (n_steps > 0) {
+    load_kv(R, kh, vh, step_key0(0), N, tid);
+    store_kv(R, Ks[0], Vt[0], tid);
+  }
+  if (n_steps > 1) load_kv(R, kh, vh, step_key0(1), N, tid);
+  __syncthreads();
 
   for (int i = 0; i < n_steps; ++i) {
+    const int cur = i & 1;
     const int k0 = step_key0(i);
-    __syncthreads();
-    store_kv(R, Ks, Vt, tid);
-    __syncthreads();
-    if (i + 1 < n_steps) load_kv(R, kh, vh, step_key0(i + 1), N, tid);
-
     const bool active = (MODE == kDenseFull) || (k0 <= qw0 + 31);
-    if (!active || qw0 >= N) continue;
-
-    // S^T = K Q^T for the 64 keys (two 32-key tiles).
-    f32x16 sacc[2];
+    if (active && qw0 < N) {
+      const uint16_t* Kc = Ks[cur];
+      const uint16_t* Vc = Vt[cur];
+      // S^T = K Q^T for the 64 keys (two 32-key tiles).
+      f32x16 sacc[2];
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+      for (int u = 0; u < 2; ++u) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[u][r] = 0.0f;
+        for (int r = 0; r < 16; ++r) sacc[u][r] = 0.0f;
 #pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        const bf16x8 a = as_bf16x8(*(const uint4*)(Ks + (32 * u + jq) * kKStride + 16 * s + 8 * hf));
-        sacc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[s], sacc[u], 0, 0, 0);
-      }
-    }
-    // scale into base-2 logits, mask future / out-of-range keys
-    const bool need_mask = (MODE != kDenseFull && k0 + kSub - 1 > qw0) || (k0 + kSub > N);
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float sv = sacc[u][r] * sc_log2;
-        if (need_mask) {
-          const int key = k0 + 32 * u + 8 * (r >> 2) + 4 * hf + (r & 3);
-          if (key >= N || (MODE != kDenseFull && key > qrow)) sv = -INFINITY;
+        for (int s = 0; s < 8; ++s) {
+          const bf16x8 a = as_bf16x8(*(const uint4*)(Kc + (32 * u + jq) * kKStride + 16 * s + 8 * hf));
+          sacc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[s], sacc[u], 0, 0, 0);
         }
-        sacc[u][r] = sv;
       }
-    float mx = -INFINITY;
+      // mask keys after the query (causal) or at / past N; branch-free
+      const bool need_mask = (MODE != kDenseFull && k0 + kSub - 1 > qw0) || (k0 + kSub > N);
+      if (need_mask) {
+        const int lim = (MODE == kDenseFull ? N - 1 : min(qrow, N - 1)) - k0 - 4 * hf;
 #pragma unroll
-    for (int u = 0; u < 2; ++u)
+        for (int u = 0; u < 2; ++u)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[u][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_i, mx);
-    const float m_use = (m_new == -INFINITY) ? 0.0f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(m_i - m_use);
-    float lsum = 0.0f;
-    uint4 pw[4];   // P^T as bf16, one 16-key MFMA step each
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const int u = s >> 1, base = 8 * (s & 1);
-      float p[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        p[e] = __builtin_amdgcn_exp2f(sacc[u][base + e] - m_use);
-        lsum += p[e];
+          for (int r = 0; r < 16; ++r) {
+            const int kk = 32 * u + 8 * (r >> 2) + (r & 3);
+            sacc[u][r] = (kk <= lim) ? sacc[u][r] : -INFINITY;
+          }
       }
-      pw[s] = make_uint4(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
-                         pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7]));
-    }
-    l_i = l_i * alpha + lsum;
-    m_i = m_new;
+      float mx = -INFINITY;
 #pragma unroll
-    for (int d = 0; d < 4; ++d)
+      for (int u = 0; u < 2; ++u)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[d][r] *= alpha;
-    // O^T += V^T P^T
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[u][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mcand = mx * sc_log2;
+      if (__builtin_amdgcn_ballot_w64(mcand > m_i + kRescaleThreshold) != 0) {
+        const float m_new = fmaxf(m_i, mcand);
+        const float alpha = (m_new == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f(m_i - m_new);
+        l_i *= alpha;
 #pragma unroll
-    for (int d = 0; d < 4; ++d) {
+        for (int d = 0; d < 4; ++d)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[d][r] *= alpha;
+        m_i = m_new;
+      }
+      const float mneg = (m_i == -INFINITY) ? 0.0f : -m_i;
+      uint4 pw[4];   // P^T as bf16, one 16-key MFMA step each
+      float lsum = 0.0f;
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
-        const bf16x8 a = as_bf16x8(*(const uint4*)(Vt + (32 * d + jq) * kVStride + 16 * s + 8 * hf));
-        oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(pw[s]), oacc[d], 0, 0, 0);
+        const int u = s >> 1, base = 8 * (s & 1);
+        float p[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          p[e] = __builtin_amdgcn_exp2f(fmaf(sacc[u][base + e], sc_log2, mneg));
+          lsum += p[e];
+        }
+        pw[s] = make_uint4(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
+                           pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7]));
+      }
+      l_i += lsum;
+      // O^T += V^T P^T
+#pragma unroll
+      for (int d = 0; d < 4; ++d) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          const bf16x8 a = as_bf16x8(*(const uint4*)(Vc + (32 * d + jq) * kVStride + 16 * s + 8 * hf));
+          oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(pw[s]), oacc[d], 0, 0, 0);
+        }
       }
     }
+    if (i + 1 < n_steps) store_kv(R, Ks[cur ^ 1], Vt[cur ^ 1], tid);
+    if (i + 2 < n_steps) load_kv(R, kh, vh, step_key0(i + 2), N, tid);
+    __syncthreads();
   }
 
   if (qrow >= N) return;
@@ -272,16 +342,16 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(
     }
 }
 
-template <int MODE>
+template <int MODE, int SUB>
 hipError_t launch_t(const uint16_t* q, const uint16_t* k, const uint16_t* v, const AttnShape& s,
                     const int32_t* bidx, const int32_t* bcnt, uint16_t* o, hipStream_t stream) {
   const int n_tiles = (s.N + kTileQ - 1) / kTileQ;
   const int64_t total = (int64_t)s.B * s.Hq * n_tiles;
   const int64_t grid = (total + kXcds - 1) / kXcds * kXcds;
   const float sc_log2 = (float)((double)s.softmax_scale * 1.4426950408889634);
-  hipLaunchKernelGGL(attn_kernel<MODE>, dim3((unsigned)grid), dim3(kThreads), 0, stream, q, k, v,
-                     o, s.B, s.Hq, s.Hkv, s.N, n_tiles, s.Ls, s.Lb / kSub, s.CS, s.CB, sc_log2,
-                     bidx, bcnt, s.kmax);
+  hipLaunchKernelGGL((attn_kernel<MODE, SUB>), dim3((unsigned)grid), dim3(kThreads), 0, stream,
+                     q, k, v, o, s.B, s.Hq, s.Hkv, s.N, n_tiles, s.Ls, s.CS, s.CB, sc_log2, bidx,
+                     bcnt, s.kmax);
   return hipGetLastError();
 }
 
@@ -290,10 +360,16 @@ hipError_t launch_t(const uint16_t* q, const uint16_t* k, const uint16_t* v, con
 hipError_t launch_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                             const AttnShape& s, AttnMode mode, const int32_t* block_idx,
                             const int32_t* block_cnt, uint16_t* o, hipStream_t stream) {
+  if (s.B * (int64_t)s.Hq * ((s.N + kTileQ - 1) / kTileQ) >= (int64_t)1 << 31)
+    return hipErrorInvalidValue;
   switch (mode) {
-    case kSparse: return launch_t<kSparse>(q, k, v, s, block_idx, block_cnt, o, stream);
-    case kDenseCausal: return launch_t<kDenseCausal>(q, k, v, s, nullptr, nullptr, o, stream);
-    default: return launch_t<kDenseFull>(q, k, v, s, nullptr, nullptr, o, stream);
+    case kSparse:
+      return s.Lb == 2 * kSub
+                 ? launch_t<kSparse, 2>(q, k, v, s, block_idx, block_cnt, o, stream)
+                 : launch_t<kSparse, 1>(q, k, v, s, block_idx, block_cnt, o, stream);
+    case kDenseCausal:
+      return launch_t<kDenseCausal, 1>(q, k, v, s, nullptr, nullptr, o, stream);
+    default: return launch_t<kDenseFull, 1>(q, k, v, s, nullptr, nullptr, o, stream);
   }
 }
 
