@@ -3,8 +3,9 @@
 // full-attention baseline).
 //
 // One workgroup = one 128-row query tile of one (batch, query head); four
-// waves own 32 query rows each.  Keys are visited in 64-key sub-blocks staged
-// through LDS (K row-major, V transposed); per sub-block each wave computes
+// waves own 32 query rows each.  Keys are visited in 64-key sub-blocks copied
+// straight from global memory into a two-stage LDS ring (no register
+// staging); per sub-block each wave computes
 //   S^T = K Q^T        2 x 8  MFMA 32x32x16 (keys on M, queries on N)
 //   online softmax     fp32, base 2, the row of one query lives in one lane
 //                      pair (lanes l and l^32)
@@ -17,9 +18,10 @@
 //   A[i][k]: lane holds i = l % 32, k = 8h .. 8h+7
 //   B[k][j]: lane holds j = l % 32, k = 8h .. 8h+7
 //   D[i][j]: lane holds j = l % 32, i = 8 (r / 4) + 4h + r % 4, r = 0..15
-// The keys of the S^T output a lane holds are therefore not contiguous; V is
-// stored in LDS with the matching key permutation so that P^T can be fed to
-// the second product straight from registers.
+// The keys of the S^T output a lane holds are therefore not contiguous; the
+// V^T operand is read from the row-major V tile with the transposing LDS read
+// (ds_read_b64_tr_b16) in that same key order, so P^T feeds the second
+// product straight from registers.
 //
 // Dense workgroups are mapped so that each XCD (dispatched round-robin)
 // receives a contiguous run of (batch, KV head, tile, query head) work: the G
@@ -44,8 +46,6 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 constexpr int kThreads = 256;
 constexpr int kTileQ = 128;
 constexpr int kSub = 64;            // keys per staged sub-block
-constexpr int kKStride = 136;       // K row stride in LDS (bf16), padded
-constexpr int kVStride = 72;        // V^T row stride in LDS (bf16), padded
 constexpr int kXcds = 8;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 w) { return __builtin_bit_cast(bf16x8, w); }
@@ -56,71 +56,85 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(x, bf16x2));
 }
 
-// Position of key quad m (keys 4m .. 4m+3 of a 64-key sub-block) in the
-// permuted V^T row: within each 16-key group, key 8a + 4h + q sits at 8h + 4a + q.
-__device__ __forceinline__ int vquad_pos(int m) {
-  return 16 * (m >> 2) + 8 * (m & 1) + 4 * ((m >> 1) & 1);
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
+
+// One LDS stage holds a 64-key sub-block of K and of V, each row-major with
+// 256-byte rows and the 16-byte chunks of row r XOR-swizzled by r % 16, so
+// that the MFMA operand reads of 8 or 16 consecutive rows hit distinct banks.
+constexpr int kRowBytes = kHeadDim * 2;
+constexpr int kTileBytes = kSub * kRowBytes;       // 16 KiB
+constexpr int kStageBytes = 2 * kTileBytes;        // K then V
+
+__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ (row & 15); }
+
+// 16 bytes per lane from global memory straight into LDS at lds_base + 16 *
+// lane (global_load_lds_dwordx4; M0 holds the LDS base and is restored).
+// Written as asm so that the compiler does not treat the copy as a pending
+// LDS write before every later LDS read: completion is enforced explicitly
+// with a vmcnt wait before the barrier that publishes a stage.
+__device__ __forceinline__ void copy16_to_lds(const uint16_t* src, uint32_t lds_base) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds_base), "v"(src)
+      : "memory");
 }
 
-struct KVRegs {
-  uint4 k[4];
-  uint4 v[4];
-};
-
-// Global -> registers for one 64-key sub-block starting at key k0.  Rows at
-// or past N are zero-filled (their scores are masked).
-__device__ __forceinline__ void load_kv(KVRegs& R, const uint16_t* __restrict__ kh,
-                                        const uint16_t* __restrict__ vh, int k0, int N,
-                                        int tid) {
-  const int c = tid & 15, r0 = tid >> 4;
-  const int m = tid & 15, cv = tid >> 4;
-  if (k0 + kSub <= N) {
+// Global -> LDS without registers: each wave moves 16 rows of K and 16 rows
+// of V (4 + 4 instructions of 64 lanes x 16 bytes).  Lane L of instruction j
+// fills row 16 w + 4 j + L / 16, swizzled chunk position L % 16.  Rows at or
+// past N are read from row N - 1 (finite data whose scores are masked).
+__device__ __forceinline__ void issue_stage(unsigned char* stage, const uint16_t* __restrict__ kh,
+                                            const uint16_t* __restrict__ vh, int k0, int N,
+                                            int wave, int lane) {
+  const int pos = lane & 15;
+  const uint32_t base = (uint32_t)(uintptr_t)stage;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      R.k[i] = *(const uint4*)(kh + (size_t)(k0 + r0 + 16 * i) * kHeadDim + 8 * c);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      R.v[i] = *(const uint4*)(vh + (size_t)(k0 + 4 * m + i) * kHeadDim + 8 * cv);
-  } else {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = k0 + r0 + 16 * i;
-      R.k[i] = row < N ? *(const uint4*)(kh + (size_t)row * kHeadDim + 8 * c)
-                       : make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = k0 + 4 * m + i;
-      R.v[i] = row < N ? *(const uint4*)(vh + (size_t)row * kHeadDim + 8 * cv)
-                       : make_uint4(0, 0, 0, 0);
-    }
+  for (int j = 0; j < 4; ++j) {
+    const int row = 16 * wave + 4 * j + (lane >> 4);
+    const int grow = min(k0 + row, N - 1);
+    const int chunk = swz(row, pos);
+    const size_t off = (size_t)grow * kHeadDim + 8 * chunk;
+    const uint32_t dst = base + (uint32_t)((16 * wave + 4 * j) * kRowBytes);
+    copy16_to_lds(kh + off, __builtin_amdgcn_readfirstlane(dst));
+    copy16_to_lds(vh + off, __builtin_amdgcn_readfirstlane(dst + kTileBytes));
   }
 }
 
-// Registers -> LDS: K row-major; V transposed (head dim major) with the key
-// permutation above, packing each dim of a key quad with two byte permutes.
-__device__ __forceinline__ void store_kv(const KVRegs& R, uint16_t* Ks, uint16_t* Vt, int tid) {
-  const int c = tid & 15;
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-    *(uint4*)(Ks + ((tid >> 4) + 16 * i) * kKStride + 8 * c) = R.k[i];
-  const int m = tid & 15, cv = tid >> 4;
-  uint16_t* vb = Vt + (8 * cv) * kVStride + vquad_pos(m);
-  const uint32_t w0[4] = {R.v[0].x, R.v[0].y, R.v[0].z, R.v[0].w};
-  const uint32_t w1[4] = {R.v[1].x, R.v[1].y, R.v[1].z, R.v[1].w};
-  const uint32_t w2[4] = {R.v[2].x, R.v[2].y, R.v[2].z, R.v[2].w};
-  const uint32_t w3[4] = {R.v[3].x, R.v[3].y, R.v[3].z, R.v[3].w};
-#pragma unroll
-  for (int qd = 0; qd < 4; ++qd) {
-    // dims 8 cv + 2 qd (low halves) and 8 cv + 2 qd + 1 (high halves)
-    const uint32_t lo01 = __builtin_amdgcn_perm(w1[qd], w0[qd], 0x05040100u);
-    const uint32_t lo23 = __builtin_amdgcn_perm(w3[qd], w2[qd], 0x05040100u);
-    const uint32_t hi01 = __builtin_amdgcn_perm(w1[qd], w0[qd], 0x07060302u);
-    const uint32_t hi23 = __builtin_amdgcn_perm(w3[qd], w2[qd], 0x07060302u);
-    *(uint2*)(vb + (2 * qd) * kVStride) = make_uint2(lo01, lo23);
-    *(uint2*)(vb + (2 * qd + 1) * kVStride) = make_uint2(hi01, hi23);
-  }
+// K operand of S^T = K Q^T: 8 bf16 of key row `row`, dims 16 s + 8 h .. +7.
+__device__ __forceinline__ bf16x8 read_k(const unsigned char* stage, int row, int s, int h) {
+  return as_bf16x8(*(const uint4*)(stage + row * kRowBytes + 16 * swz(row, 2 * s + h)));
 }
+
+// V^T operand of O^T += V^T P^T for head-dim tile dt and 16-key step t, read
+// transposed from the row-major V tile: lane l (group g = l / 16, i = l % 16)
+// receives V[key][32 dt + 16 (g % 2) + i] for the keys 16 t + 8 a + 4 (g / 2)
+// + 0..3, a = 0, 1 -- the key order of the S^T output.
+__device__ __forceinline__ bf16x8 read_vt(const unsigned char* stage, int dt, int t, int lane) {
+  const int g = lane >> 4, i = lane & 15;
+  const int d = 32 * dt + 16 * (g & 1) + 4 * (i & 3);
+  const unsigned char* vt = stage + kTileBytes;
+  s16x4 r[2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+    const int row = 16 * t + 8 * a + 4 * (g >> 1) + (i >> 2);
+    const unsigned char* p = vt + row * kRowBytes + 16 * swz(row, d >> 3) + 2 * (d & 7);
+    r[a] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)p);
+  }
+  const uint2 lo = __builtin_bit_cast(uint2, r[0]), hi = __builtin_bit_cast(uint2, r[1]);
+  return as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
+}
+
+// Wait until at most n vector-memory operations of this wave are in flight
+// (gfx9 encoding: vmcnt in bits 3:0 and 15:14; expcnt, lgkmcnt left at max).
+#define EI_WAIT_VMCNT(n) \
+  __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (7 << 4) | (15 << 8))
 
 // Lazy rescaling: the running maximum is only raised when a new score exceeds
 // it by more than 2^8 (base-2 units), so exp2 arguments stay <= 8 and O, l are
@@ -134,8 +148,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(
     const uint16_t* __restrict__ v, uint16_t* __restrict__ o, int B, int Hq, int Hkv, int N,
     int n_tiles, int Ls, int CS, int CB, float sc_log2, const int32_t* __restrict__ bidx,
     const int32_t* __restrict__ bcnt, int kmax) {
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kSub * kKStride];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][kHeadDim * kVStride];
+  // two LDS objects (not one array) so that the compiler can tell the copy
+  // into one stage from the reads of the other
+  __shared__ __attribute__((aligned(1024))) unsigned char stage0[kStageBytes];
+  __shared__ __attribute__((aligned(1024))) unsigned char stage1[kStageBytes];
 
   const unsigned G = (unsigned)(Hq / Hkv);
   const unsigned total = (unsigned)B * (unsigned)Hq * (unsigned)n_tiles;
@@ -240,21 +256,16 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(
     for (int r = 0; r < 16; ++r) oacc[d][r] = 0.0f;
   float m_i = -INFINITY, l_i = 0.0f;
 
-  KVRegs R;
-  if (n_steps > 0) {
-    load_kv(R, kh, vh, step_key0(0), N, tid);
-    store_kv(R, Ks[0], Vt[0], tid);
-  }
-  if (n_steps > 1) load_kv(R, kh, vh, step_key0(1), N, tid);
-  __syncthreads();
-
-  for (int i = 0; i < n_steps; ++i) {
-    const int cur = i & 1;
+  // Two-stage LDS ring filled directly from global memory.  Step i waits for
+  // its stage (the 8 loads of step i+1 may still be in flight), computes, and
+  // after a second barrier refills the stage with step i+2.  Even steps use
+  // stage0, odd steps stage1.
+  auto step = [&](const int i, unsigned char* st) {
+    if (i + 1 < n_steps) EI_WAIT_VMCNT(8); else EI_WAIT_VMCNT(0);
+    __syncthreads();
     const int k0 = step_key0(i);
     const bool active = (MODE == kDenseFull) || (k0 <= qw0 + 31);
     if (active && qw0 < N) {
-      const uint16_t* Kc = Ks[cur];
-      const uint16_t* Vc = Vt[cur];
       // S^T = K Q^T for the 64 keys (two 32-key tiles).
       f32x16 sacc[2];
 #pragma unroll
@@ -262,10 +273,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(
 #pragma unroll
         for (int r = 0; r < 16; ++r) sacc[u][r] = 0.0f;
 #pragma unroll
-        for (int s = 0; s < 8; ++s) {
-          const bf16x8 a = as_bf16x8(*(const uint4*)(Kc + (32 * u + jq) * kKStride + 16 * s + 8 * hf));
-          sacc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[s], sacc[u], 0, 0, 0);
-        }
+        for (int s = 0; s < 8; ++s)
+          sacc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(read_k(st, 32 * u + jq, s, hf), qf[s],
+                                                           sacc[u], 0, 0, 0);
       }
       // mask keys after the query (causal) or at / past N; branch-free
       const bool need_mask = (MODE != kDenseFull && k0 + kSub - 1 > qw0) || (k0 + kSub > N);
@@ -314,17 +324,25 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(
       l_i += lsum;
       // O^T += V^T P^T
 #pragma unroll
-      for (int d = 0; d < 4; ++d) {
+      for (int d = 0; d < 4; ++d)
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          const bf16x8 a = as_bf16x8(*(const uint4*)(Vc + (32 * d + jq) * kVStride + 16 * s + 8 * hf));
-          oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(pw[s]), oacc[d], 0, 0, 0);
-        }
-      }
+        for (int s = 0; s < 4; ++s)
+          oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(read_vt(st, d, s, lane),
+                                                           as_bf16x8(pw[s]), oacc[d], 0, 0, 0);
     }
-    if (i + 1 < n_steps) store_kv(R, Ks[cur ^ 1], Vt[cur ^ 1], tid);
-    if (i + 2 < n_steps) load_kv(R, kh, vh, step_key0(i + 2), N, tid);
-    __syncthreads();
+    if (i + 2 < n_steps) {
+      __syncthreads();   // every wave is done reading this stage
+      issue_stage(st, kh, vh, step_key0(i + 2), N, wave, lane);
+    }
+  };
+  // Q fragments (and the list) have landed before any stage copy is issued,
+  // so no later wait on them covers the copies in flight.
+  EI_WAIT_VMCNT(0);
+  if (n_steps > 0) issue_stage(stage0, kh, vh, step_key0(0), N, wave, lane);
+  if (n_steps > 1) issue_stage(stage1, kh, vh, step_key0(1), N, wave, lane);
+  for (int i = 0; i < n_steps; i += 2) {
+    step(i, stage0);
+    if (i + 1 < n_steps) step(i + 1, stage1);
   }
 
   if (qrow >= N) return;

@@ -13,8 +13,9 @@
 //                 4 logits of every query head of the chunk in binary64 FMA
 //                 (products of bf16 values are exact, so the logits equal the
 //                 plain definition's); it keeps fp32 offsets from a per-wave
-//                 reference in LDS, then one wave per query head evaluates the
-//                 four softmaxes, A = max((S1+S2)/2, (S3+S4)/2) and
+//                 reference in LDS; then one wave per logit row finds the
+//                 row's maximum, argmax and log-sum-exp, and the waves of
+//                 each head evaluate A = max((S1+S2)/2, (S3+S4)/2) and
 //                 H = -sum A ln A in log space (fp32 terms, fp64 sums).
 #include "ei_internal.h"
 
@@ -122,17 +123,29 @@ __device__ __forceinline__ float log_pair_avg(float a, float b) {
   return hi + log1pf(expf(lo - hi)) - 0.69314718055994531f;
 }
 
-// HPW query heads per workgroup; rows of the score block: 4 logit products
-// (S1..S4) per head.
-template <int HPW>
-__global__ __launch_bounds__(kThreads) void scores_kernel(
+// Per-row statistics of the four softmaxes, kept in LDS between phases.
+struct RowStats {
+  float M;       // max of the per-wave references
+  float best;    // largest offset (the argmax's)
+  int bj;        // argmax (lowest index among equal offsets)
+  float lse;     // log1p(rest), rest = sum over j != argmax of exp(x_j - x_argmax)
+  double dfc;    // 1 - S[argmax] = rest / (1 + rest)
+};
+
+// HPW query heads per workgroup of NT threads; rows of the score block: the 4
+// logit products (S1..S4) of each head.
+template <int HPW, int NT>
+__global__ __launch_bounds__(NT) void scores_kernel(
     const double* __restrict__ qrep, const uint16_t* __restrict__ krep,
     float* __restrict__ log_scores, float* __restrict__ entropy, int Hq, int Hkv, int CS,
     int CB, int r, int s_lo, int s_hi, int n_hc, int ldy, double probe_scale) {
   constexpr int R = 4 * HPW;
-  extern __shared__ float smem[];
-  float* ys = smem;                 // [R][ldy] fp32 offsets x - ref
-  float* refs = smem + R * ldy;     // [R][ldy / 64] per-wave references
+  constexpr int W = NT / kWave;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
+  RowStats* stats = (RowStats*)smem_raw;                        // [R]
+  double* hpart = (double*)(smem_raw + sizeof(RowStats) * R);   // [W]
+  float* ys = (float*)(hpart + W);                              // [R][ldy] offsets x - ref
+  float* refs = ys + R * ldy;                                   // [R][ldy / 64] references
   const int nref = ldy >> 6;
 
   int64_t id = blockIdx.x;
@@ -156,7 +169,7 @@ __global__ __launch_bounds__(kThreads) void scores_kernel(
   const uint16_t* kb = krep + (size_t)(b * Hkv + g) * CB * 2 * kHeadDim;
 
   // Phase 1: exact logits, one key block per lane.
-  for (int j0 = wave * kWave; j0 < nvis; j0 += kThreads) {
+  for (int j0 = wave * kWave; j0 < nvis; j0 += NT) {
     const int j = j0 + lane;
     const bool valid = j < nvis;
     const uint16_t* kr = kb + (size_t)(valid ? j : nvis - 1) * 2 * kHeadDim;
@@ -196,77 +209,71 @@ __global__ __launch_bounds__(kThreads) void scores_kernel(
   }
   __syncthreads();
 
-  // Phase 2: one wave per query head.
-  for (int hh = wave; hh < nh; hh += kWavesPerBlock) {
+  // Phase 2a: statistics of every logit row, one wave per row.
+  const int nch = (nvis + 63) >> 6;
+  for (int row = wave; row < 4 * nh; row += W) {
+    const float* yr = ys + row * ldy;
+    const float* rr = refs + row * nref;
+    float m = -INFINITY;
+    for (int c = lane; c < nch; c += kWave) m = fmaxf(m, rr[c]);
+    const float M = wave_max_f32(m);
+    float best = -INFINITY;
+    int bj = 0x7fffffff;
+    for (int j = lane; j < nvis; j += kWave) {
+      const float dv = yr[j] + (rr[j >> 6] - M);
+      if (dv > best) { best = dv; bj = j; }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ob = __shfl_xor(best, o);
+      const int oj = __shfl_xor(bj, o);
+      if (ob > best || (ob == best && oj < bj)) { best = ob; bj = oj; }
+    }
+    double rest = 0.0;
+    for (int j = lane; j < nvis; j += kWave) {
+      const float dv = yr[j] + (rr[j >> 6] - M);
+      if (j != bj) rest += (double)expf(dv - best);
+    }
+    rest = wave_sum_f64(rest);
+    if (lane == 0) stats[row] = RowStats{M, best, bj, (float)log1p(rest), rest / (1.0 + rest)};
+  }
+  __syncthreads();
+
+  // Phase 2b: ln A and the entropy terms; each head's row is split over
+  // W / HPW waves.
+  constexpr int P = W / HPW;
+  const int hh = wave % HPW, part = wave / HPW;
+  double H = 0.0;
+  if (hh < nh) {
     const int h = h0 + hh;
-    const int nch = (nvis + 63) >> 6;
-    float M[4];
+    RowStats st[4];
 #pragma unroll
-    for (int cc = 0; cc < 4; ++cc) {
-      float m = -INFINITY;
-      for (int c = lane; c < nch; c += kWave) m = fmaxf(m, refs[(hh * 4 + cc) * nref + c]);
-      M[cc] = wave_max_f32(m);
-    }
-    // offsets from the row maximum: diff_c[j] = y + (ref_chunk - M_c)
-    float best[4];
-    int bj[4];
-#pragma unroll
-    for (int cc = 0; cc < 4; ++cc) { best[cc] = -INFINITY; bj[cc] = 0x7fffffff; }
-    for (int j = lane; j < nvis; j += kWave) {
-#pragma unroll
-      for (int cc = 0; cc < 4; ++cc) {
-        const int row = hh * 4 + cc;
-        const float dv = ys[row * ldy + j] + (refs[row * nref + (j >> 6)] - M[cc]);
-        if (dv > best[cc]) { best[cc] = dv; bj[cc] = j; }
-      }
-    }
-#pragma unroll
-    for (int cc = 0; cc < 4; ++cc) {
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) {
-        const float ob = __shfl_xor(best[cc], o);
-        const int oj = __shfl_xor(bj[cc], o);
-        if (ob > best[cc] || (ob == best[cc] && oj < bj[cc])) { best[cc] = ob; bj[cc] = oj; }
-      }
-    }
-    // rest_c = sum over j != argmax of exp(x_j - x_argmax)
-    double rest[4] = {0.0, 0.0, 0.0, 0.0};
-    for (int j = lane; j < nvis; j += kWave) {
-#pragma unroll
-      for (int cc = 0; cc < 4; ++cc) {
-        const int row = hh * 4 + cc;
-        const float dv = ys[row * ldy + j] + (refs[row * nref + (j >> 6)] - M[cc]);
-        if (j != bj[cc]) rest[cc] += (double)expf(dv - best[cc]);
-      }
-    }
-    double lse[4], dfc[4];
-#pragma unroll
-    for (int cc = 0; cc < 4; ++cc) {
-      rest[cc] = wave_sum_f64(rest[cc]);
-      lse[cc] = log1p(rest[cc]);
-      dfc[cc] = rest[cc] / (1.0 + rest[cc]);
-    }
-    const float lsef[4] = {(float)lse[0], (float)lse[1], (float)lse[2], (float)lse[3]};
+    for (int cc = 0; cc < 4; ++cc) st[cc] = stats[hh * 4 + cc];
+    const float l12_top = (st[0].bj == st[1].bj) ? (float)log1p(-0.5 * (st[0].dfc + st[1].dfc)) : 0.f;
+    const float l34_top = (st[2].bj == st[3].bj) ? (float)log1p(-0.5 * (st[2].dfc + st[3].dfc)) : 0.f;
     float* Lrow = log_scores + ((size_t)(b * Hq + h) * CS + s) * CB;
-    double H = 0.0;
-    for (int j = lane; j < nvis; j += kWave) {
+    for (int j = part * kWave + lane; j < nvis; j += P * kWave) {
       float ls[4];
 #pragma unroll
       for (int cc = 0; cc < 4; ++cc) {
         const int row = hh * 4 + cc;
-        const float dv = ys[row * ldy + j] + (refs[row * nref + (j >> 6)] - M[cc]);
-        ls[cc] = (j == bj[cc]) ? -lsef[cc] : (dv - best[cc]) - lsef[cc];
+        const float dv = ys[row * ldy + j] + (refs[row * nref + (j >> 6)] - st[cc].M);
+        ls[cc] = (j == st[cc].bj) ? -st[cc].lse : (dv - st[cc].best) - st[cc].lse;
       }
-      const float l12 = (j == bj[0] && j == bj[1]) ? (float)log1p(-0.5 * (dfc[0] + dfc[1]))
-                                                   : log_pair_avg(ls[0], ls[1]);
-      const float l34 = (j == bj[2] && j == bj[3]) ? (float)log1p(-0.5 * (dfc[2] + dfc[3]))
-                                                   : log_pair_avg(ls[2], ls[3]);
+      const float l12 = (j == st[0].bj && j == st[1].bj) ? l12_top : log_pair_avg(ls[0], ls[1]);
+      const float l34 = (j == st[2].bj && j == st[3].bj) ? l34_top : log_pair_avg(ls[2], ls[3]);
       const float L = fmaxf(l12, l34);
       Lrow[j] = L;
       H -= (double)(expf(L) * L);
     }
     H = wave_sum_f64(H);
-    if (lane == 0) entropy[(size_t)(b * Hq + h) * CS + s] = (float)H;
+  }
+  if (lane == 0) hpart[wave] = H;
+  __syncthreads();
+  if ((int)threadIdx.x < nh) {
+    double Ht = 0.0;
+    for (int p = 0; p < P; ++p) Ht += hpart[p * HPW + threadIdx.x];
+    entropy[(size_t)(b * Hq + h0 + threadIdx.x) * CS + s] = (float)Ht;
   }
 }
 
@@ -274,17 +281,22 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 constexpr size_t kMaxLds = 160 * 1024;
 
-size_t scores_lds_bytes(int hpw, int ldy) {
+size_t scores_lds_bytes(int hpw, int nt, int ldy) {
   const size_t R = 4 * (size_t)hpw;
-  return R * (size_t)ldy * 4 + R * (size_t)(ldy / 64) * 4;
+  return sizeof(RowStats) * R + sizeof(double) * (size_t)(nt / kWave) + R * (size_t)ldy * 4 +
+         R * (size_t)(ldy / 64) * 4;
 }
+
+// Threads per workgroup grow with the row length so that long rows keep
+// several waves per SIMD in flight.
+int pick_threads(int ldy) { return ldy <= 512 ? 256 : (ldy <= 1024 ? 512 : 1024); }
 
 // Heads per workgroup: up to 4 query heads of one KV group share each K
 // representation load; fewer when the LDS tile for this row length would
 // not fit.  0 if even one head does not fit.
 int pick_hpw(int G, int ldy, size_t max_lds) {
   int hpw = G >= 4 ? 4 : (G >= 2 ? 2 : 1);
-  while (hpw >= 1 && scores_lds_bytes(hpw, ldy) > max_lds) hpw /= 2;
+  while (hpw >= 1 && scores_lds_bytes(hpw, pick_threads(ldy), ldy) > max_lds) hpw /= 2;
   return hpw;
 }
 
@@ -297,18 +309,35 @@ size_t device_max_lds() {
   return (size_t)v < kMaxLds ? (size_t)v : kMaxLds;
 }
 
-template <int HPW>
+template <int HPW, int NT>
 hipError_t launch_scores_t(const double* qrep, const uint16_t* krep, float* log_scores,
                            float* entropy, const ProbeShape& s, int s_lo, int s_hi, int ldy,
                            double probe_scale, hipStream_t stream) {
   const int G = s.Hq / s.Hkv;
   const int n_hc = (G + HPW - 1) / HPW;
   const int64_t grid = (int64_t)s.B * s.Hkv * n_hc * (s_hi - s_lo);
-  const size_t lds = scores_lds_bytes(HPW, ldy);
-  hipLaunchKernelGGL(scores_kernel<HPW>, dim3((unsigned)grid), dim3(kThreads), lds, stream, qrep,
-                     krep, log_scores, entropy, s.Hq, s.Hkv, s.CS, s.CB, s.r, s_lo, s_hi, n_hc,
-                     ldy, probe_scale);
+  const size_t lds = scores_lds_bytes(HPW, NT, ldy);
+  hipLaunchKernelGGL((scores_kernel<HPW, NT>), dim3((unsigned)grid), dim3(NT), lds, stream,
+                     qrep, krep, log_scores, entropy, s.Hq, s.Hkv, s.CS, s.CB, s.r, s_lo, s_hi,
+                     n_hc, ldy, probe_scale);
   return hipGetLastError();
+}
+
+template <int HPW>
+hipError_t launch_scores_h(const double* qrep, const uint16_t* krep, float* log_scores,
+                           float* entropy, const ProbeShape& s, int s_lo, int s_hi, int ldy,
+                           double probe_scale, hipStream_t stream) {
+  switch (pick_threads(ldy)) {
+    case 256:
+      return launch_scores_t<HPW, 256>(qrep, krep, log_scores, entropy, s, s_lo, s_hi, ldy,
+                                       probe_scale, stream);
+    case 512:
+      return launch_scores_t<HPW, 512>(qrep, krep, log_scores, entropy, s, s_lo, s_hi, ldy,
+                                       probe_scale, stream);
+    default:
+      return launch_scores_t<HPW, 1024>(qrep, krep, log_scores, entropy, s, s_lo, s_hi, ldy,
+                                        probe_scale, stream);
+  }
 }
 
 }  // namespace
@@ -355,13 +384,13 @@ hipError_t launch_probe(const uint16_t* q, const uint16_t* k, const ProbeShape& 
     const int hpw = pick_hpw(G, ldy, max_lds);
     hipError_t e = hipErrorInvalidValue;
     if (hpw == 4)
-      e = launch_scores_t<4>(qrep, krep, log_scores, entropy, s, s_lo, s_hi, ldy, probe_scale,
+      e = launch_scores_h<4>(qrep, krep, log_scores, entropy, s, s_lo, s_hi, ldy, probe_scale,
                              stream);
     else if (hpw == 2)
-      e = launch_scores_t<2>(qrep, krep, log_scores, entropy, s, s_lo, s_hi, ldy, probe_scale,
+      e = launch_scores_h<2>(qrep, krep, log_scores, entropy, s, s_lo, s_hi, ldy, probe_scale,
                              stream);
     else if (hpw == 1)
-      e = launch_scores_t<1>(qrep, krep, log_scores, entropy, s, s_lo, s_hi, ldy, probe_scale,
+      e = launch_scores_h<1>(qrep, krep, log_scores, entropy, s, s_lo, s_hi, ldy, probe_scale,
                              stream);
     if (e != hipSuccess) return e;
     s_lo = s_hi;
