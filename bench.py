@@ -86,6 +86,9 @@ def main():
     ap.add_argument("--dense-reps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=20.0)
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="also run one device-to-device copy of this size, so that a "
+                         "rocprofv3 --pmc run can scale FETCH_SIZE / WRITE_SIZE by it")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -111,6 +114,16 @@ def main():
         return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
 
     q, k, v = to_dev(w.q), to_dev(w.k), to_dev(w.v)
+    if args.calibrate_copy_mib > 0:
+        n = args.calibrate_copy_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"[bench] calibration copy of {args.calibrate_copy_mib} MiB done", file=sys.stderr,
+              flush=True)
+        del src, dst
     bufs = {
         "log_scores": torch.empty((w.B, w.Hq, w.CS, w.CB), dtype=torch.float32, device=dev),
         "entropy": torch.empty((w.B, w.Hq, w.CS), dtype=torch.float32, device=dev),

@@ -29,7 +29,7 @@
 // and reuse K/V blocks from its L2.  Sparse work per head is uneven (budgets
 // differ per head, up to 3x), so a fixed head -> XCD assignment leaves the
 // XCD with the heaviest heads finishing last; instead the KV groups rotate
-// over the XCDs from one tile to the next.  Heavier (later) tiles are issued
+// over the XCDs every 4 tiles.  Heavier (later) tiles are issued
 // first in both.
 #include "ei_internal.h"
 
@@ -47,6 +47,7 @@ constexpr int kThreads = 256;
 constexpr int kTileQ = 128;
 constexpr int kSub = 64;            // keys per staged sub-block
 constexpr int kXcds = 8;
+constexpr unsigned kRotRun = 4;    // tiles a KV group stays on one XCD (sparse)
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 w) { return __builtin_bit_cast(bf16x8, w); }
 
@@ -167,16 +168,19 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(
     g = (int)(t % (unsigned)Hkv);
     b = (int)(t / (unsigned)Hkv);
   } else if (((unsigned)B * (unsigned)Hkv) % kXcds == 0) {
-    // Tile-major, heavier tiles first; at tile t, XCD x takes the KV groups
-    // bg with (bg + t) % 8 == x (all G query heads of each), so a group's
-    // work rotates over every XCD.
+    // Tile-major, heavier tiles first; for tile rank t, XCD x takes the KV
+    // groups bg with (bg + t / kRotRun) % 8 == x (all G query heads of each):
+    // a group stays on one XCD for kRotRun consecutive tiles (which select
+    // mostly the same blocks, so they share its L2) and then moves on, so
+    // every group's work is spread over all XCDs.
     if (blockIdx.x >= total) return;
     const unsigned x = blockIdx.x % kXcds, idx = blockIdx.x / kXcds;
     const unsigned per_tile = ((unsigned)B * (unsigned)Hq) / kXcds;
     const unsigned tr = idx / per_tile, rem = idx % per_tile;
     tile = n_tiles - 1 - (int)tr;
     hh = (int)(rem % G);
-    const unsigned bg = (x + kXcds - (unsigned)tile % kXcds) % kXcds + kXcds * (rem / G);
+    const unsigned rot = (tr / kRotRun) % kXcds;
+    const unsigned bg = (x + kXcds - rot) % kXcds + kXcds * (rem / G);
     b = (int)(bg / (unsigned)Hkv);
     g = (int)(bg % (unsigned)Hkv);
   } else {
