@@ -88,7 +88,7 @@ int64_t ei_num_blocks(ei_dims dims, ei_tiling tiling);
 int32_t ei_kmax(ei_tiling tiling, ei_budget_params params);
 
 /* Workspace bytes ei_entropy_probe needs (Q representation in binary64 and
- * K representation in bf16, Algorithm 1); 0 on invalid sizes. */
+ * K representation in fp32, Algorithm 1); 0 on invalid sizes. */
 size_t ei_probe_workspace_bytes(ei_dims dims, ei_tiling tiling);
 
 /*

@@ -25,6 +25,20 @@ __device__ __forceinline__ float wave_max_f32(float v) {
   return v;
 }
 
+// Max over the 64 lanes: butterflies within rows of 16 lanes by DPP, then two
+// cross-row exchanges.
+#define EI_DPP_MOV(v, ctrl) \
+  __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, (v)), (ctrl), 0xF, 0xF, false))
+__device__ __forceinline__ float wave_max_f32_dpp(float v) {
+  v = fmaxf(v, EI_DPP_MOV(v, 0xB1));    // quad_perm [1,0,3,2]
+  v = fmaxf(v, EI_DPP_MOV(v, 0x4E));    // quad_perm [2,3,0,1]
+  v = fmaxf(v, EI_DPP_MOV(v, 0x141));   // row_half_mirror
+  v = fmaxf(v, EI_DPP_MOV(v, 0x140));   // row_mirror
+  v = fmaxf(v, __shfl_xor(v, 16));
+  v = fmaxf(v, __shfl_xor(v, 32));
+  return v;
+}
+
 __device__ __forceinline__ double wave_sum_f64(double v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);

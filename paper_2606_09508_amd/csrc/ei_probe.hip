@@ -6,8 +6,8 @@
 //  pool_kernel    streams Q and K once from HBM (the bound of the probe) and
 //                 writes Q_max/Q_min per segment in binary64 (so the scores
 //                 kernel can read them as uniform scalar operands) and
-//                 K_max/K_min per key block in bf16 (exact: pooled values are
-//                 input values).
+//                 K_max/K_min per key block in fp32 (exact: pooled values are
+//                 input values; one convert to binary64 per use).
 //  scores_kernel  one workgroup per (b, KV head, segment, chunk of query
 //                 heads).  Each lane owns one visible key block and forms the
 //                 4 logits of every query head of the chunk in binary64 FMA
@@ -30,7 +30,7 @@ constexpr int kWavesPerBlock = kThreads / kWave;
 __global__ __launch_bounds__(kThreads) void pool_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, int B, int Hq, int Hkv,
     int N, int Ls, int Lb, int CS, int CB, double* __restrict__ qrep,
-    uint16_t* __restrict__ krep) {
+    float* __restrict__ krep) {
   const int lane = threadIdx.x & (kWave - 1);
   const int64_t item = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
   const int64_t nq = (int64_t)B * Hq * CS, nk = (int64_t)B * Hkv * CB;
@@ -96,31 +96,34 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(
       *(double2*)(out + kHeadDim + e) = make_double2((double)mn[e], (double)mn[e + 1]);
     }
   } else {
-    uint16_t* out = krep + ((size_t)head * CB + grp) * 2 * kHeadDim + 8 * c;
-    uint32_t px[4], pn[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      px[e] = (__float_as_uint(mx[2 * e]) >> 16) | (__float_as_uint(mx[2 * e + 1]) & 0xffff0000u);
-      pn[e] = (__float_as_uint(mn[2 * e]) >> 16) | (__float_as_uint(mn[2 * e + 1]) & 0xffff0000u);
-    }
-    *(uint4*)out = make_uint4(px[0], px[1], px[2], px[3]);
-    *(uint4*)(out + kHeadDim) = make_uint4(pn[0], pn[1], pn[2], pn[3]);
+    float* out = krep + ((size_t)head * CB + grp) * 2 * kHeadDim + 8 * c;
+    *(float4*)out = make_float4(mx[0], mx[1], mx[2], mx[3]);
+    *(float4*)(out + 4) = make_float4(mx[4], mx[5], mx[6], mx[7]);
+    *(float4*)(out + kHeadDim) = make_float4(mn[0], mn[1], mn[2], mn[3]);
+    *(float4*)(out + kHeadDim + 4) = make_float4(mn[4], mn[5], mn[6], mn[7]);
   }
 }
 
-__device__ __forceinline__ void widen8(const uint4 w, double* out) {
-  const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    out[2 * e] = (double)bf16_lo(ww[e]);
-    out[2 * e + 1] = (double)bf16_hi(ww[e]);
-  }
+__device__ __forceinline__ void widen4(const float4 w, double* out) {
+  out[0] = (double)w.x;
+  out[1] = (double)w.y;
+  out[2] = (double)w.z;
+  out[3] = (double)w.w;
 }
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.69314718055994531f;
+
+// e^x and ln(1 + y) for y in [0, 1] on the hardware exp2 / log2 (relative
+// error ~1e-7 for the arguments used here; the one entry per row that needs
+// ln of a value near 1 is evaluated in binary64 instead).
+__device__ __forceinline__ float fast_exp(float x) { return __builtin_amdgcn_exp2f(x * kLog2e); }
+__device__ __forceinline__ float fast_log1p01(float y) { return __builtin_amdgcn_logf(1.0f + y) * kLn2; }
 
 // ln((exp(a) + exp(b)) / 2) for a, b <= 0, not both near 0.
 __device__ __forceinline__ float log_pair_avg(float a, float b) {
   const float hi = fmaxf(a, b), lo = fminf(a, b);
-  return hi + log1pf(expf(lo - hi)) - 0.69314718055994531f;
+  return hi + fast_log1p01(fast_exp(lo - hi)) - kLn2;
 }
 
 // Per-row statistics of the four softmaxes, kept in LDS between phases.
@@ -136,7 +139,7 @@ struct RowStats {
 // logit products (S1..S4) of each head.
 template <int HPW, int NT>
 __global__ __launch_bounds__(NT) void scores_kernel(
-    const double* __restrict__ qrep, const uint16_t* __restrict__ krep,
+    const double* __restrict__ qrep, const float* __restrict__ krep,
     float* __restrict__ log_scores, float* __restrict__ entropy, int Hq, int Hkv, int CS,
     int CB, int r, int s_lo, int s_hi, int n_hc, int ldy, double probe_scale) {
   constexpr int R = 4 * HPW;
@@ -166,13 +169,13 @@ __global__ __launch_bounds__(NT) void scores_kernel(
 #pragma unroll
   for (int hh = 0; hh < HPW; ++hh)
     qv[hh] = qrep + ((size_t)(b * Hq + h0 + min(hh, nh - 1)) * CS + s) * 2 * kHeadDim;
-  const uint16_t* kb = krep + (size_t)(b * Hkv + g) * CB * 2 * kHeadDim;
+  const float* kb = krep + (size_t)(b * Hkv + g) * CB * 2 * kHeadDim;
 
   // Phase 1: exact logits, one key block per lane.
   for (int j0 = wave * kWave; j0 < nvis; j0 += NT) {
     const int j = j0 + lane;
     const bool valid = j < nvis;
-    const uint16_t* kr = kb + (size_t)(valid ? j : nvis - 1) * 2 * kHeadDim;
+    const float* kr = kb + (size_t)(valid ? j : nvis - 1) * 2 * kHeadDim;
     double acc[HPW][4];
 #pragma unroll
     for (int hh = 0; hh < HPW; ++hh)
@@ -181,8 +184,10 @@ __global__ __launch_bounds__(NT) void scores_kernel(
 #pragma unroll 2
     for (int d0 = 0; d0 < kHeadDim; d0 += 8) {
       double kx[8], kn[8];
-      widen8(*(const uint4*)(kr + d0), kx);
-      widen8(*(const uint4*)(kr + kHeadDim + d0), kn);
+      widen4(*(const float4*)(kr + d0), kx);
+      widen4(*(const float4*)(kr + d0 + 4), kx + 4);
+      widen4(*(const float4*)(kr + kHeadDim + d0), kn);
+      widen4(*(const float4*)(kr + kHeadDim + d0 + 4), kn + 4);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
 #pragma unroll
@@ -201,7 +206,7 @@ __global__ __launch_bounds__(NT) void scores_kernel(
       for (int cc = 0; cc < 4; ++cc) {
         const int row = hh * 4 + cc;
         const double x = probe_scale * acc[hh][cc];
-        const float ref = wave_max_f32(valid ? (float)x : -INFINITY);
+        const float ref = wave_max_f32_dpp(valid ? (float)x : -INFINITY);
         if (valid) ys[row * ldy + j] = (float)(x - (double)ref);
         if (lane == 0) refs[row * nref + (j0 >> 6)] = ref;
       }
@@ -232,7 +237,7 @@ __global__ __launch_bounds__(NT) void scores_kernel(
     double rest = 0.0;
     for (int j = lane; j < nvis; j += kWave) {
       const float dv = yr[j] + (rr[j >> 6] - M);
-      if (j != bj) rest += (double)expf(dv - best);
+      if (j != bj) rest += (double)fast_exp(dv - best);
     }
     rest = wave_sum_f64(rest);
     if (lane == 0) stats[row] = RowStats{M, best, bj, (float)log1p(rest), rest / (1.0 + rest)};
@@ -264,7 +269,7 @@ __global__ __launch_bounds__(NT) void scores_kernel(
       const float l34 = (j == st[2].bj && j == st[3].bj) ? l34_top : log_pair_avg(ls[2], ls[3]);
       const float L = fmaxf(l12, l34);
       Lrow[j] = L;
-      H -= (double)(expf(L) * L);
+      H -= (double)(fast_exp(L) * L);
     }
     H = wave_sum_f64(H);
   }
@@ -310,7 +315,7 @@ size_t device_max_lds() {
 }
 
 template <int HPW, int NT>
-hipError_t launch_scores_t(const double* qrep, const uint16_t* krep, float* log_scores,
+hipError_t launch_scores_t(const double* qrep, const float* krep, float* log_scores,
                            float* entropy, const ProbeShape& s, int s_lo, int s_hi, int ldy,
                            double probe_scale, hipStream_t stream) {
   const int G = s.Hq / s.Hkv;
@@ -324,7 +329,7 @@ hipError_t launch_scores_t(const double* qrep, const uint16_t* krep, float* log_
 }
 
 template <int HPW>
-hipError_t launch_scores_h(const double* qrep, const uint16_t* krep, float* log_scores,
+hipError_t launch_scores_h(const double* qrep, const float* krep, float* log_scores,
                            float* entropy, const ProbeShape& s, int s_lo, int s_hi, int ldy,
                            double probe_scale, hipStream_t stream) {
   switch (pick_threads(ldy)) {
@@ -346,7 +351,7 @@ size_t probe_qrep_bytes(const ProbeShape& s) {
   return align_up((size_t)s.B * s.Hq * s.CS * 2 * kHeadDim * sizeof(double));
 }
 size_t probe_krep_bytes(const ProbeShape& s) {
-  return align_up((size_t)s.B * s.Hkv * s.CB * 2 * kHeadDim * sizeof(uint16_t));
+  return align_up((size_t)s.B * s.Hkv * s.CB * 2 * kHeadDim * sizeof(float));
 }
 
 bool probe_supported(const ProbeShape& s) {
@@ -358,7 +363,7 @@ hipError_t launch_probe(const uint16_t* q, const uint16_t* k, const ProbeShape& 
                         double probe_scale, float* log_scores, float* entropy, void* workspace,
                         hipStream_t stream) {
   double* qrep = (double*)workspace;
-  uint16_t* krep = (uint16_t*)((char*)workspace + probe_qrep_bytes(s));
+  float* krep = (float*)((char*)workspace + probe_qrep_bytes(s));
   {
     const int64_t items = (int64_t)s.B * s.Hq * s.CS + (int64_t)s.B * s.Hkv * s.CB;
     const int64_t grid = (items + kWavesPerBlock - 1) / kWavesPerBlock;
