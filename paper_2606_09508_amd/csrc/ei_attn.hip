@@ -61,13 +61,21 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
 
 // One LDS stage holds a 64-key sub-block of K and of V, each row-major with
-// 256-byte rows and the 16-byte chunks of row r XOR-swizzled by r % 16, so
-// that the MFMA operand reads of 8 or 16 consecutive rows hit distinct banks.
+// 256-byte rows whose 16-byte chunks are XOR-swizzled per row.  K rows are
+// read 16 at a time at one logical chunk, so K uses chunk ^ (r % 16).  The
+// transposing V reads take, per 16 lanes, the same 32-byte chunk pair of 4
+// consecutive rows (and per 32 lanes a 64-byte chunk quad), so V uses
+// chunk ^ h(r % 4) with h = {0, 6, 12, 10}: the pair index and the quad index
+// then differ across any 4 consecutive rows and every read is free of bank
+// conflicts.
 constexpr int kRowBytes = kHeadDim * 2;
 constexpr int kTileBytes = kSub * kRowBytes;       // 16 KiB
 constexpr int kStageBytes = 2 * kTileBytes;        // K then V
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ (row & 15); }
+__device__ __forceinline__ int swz_v(int row, int chunk) {
+  return chunk ^ ((0xAC60 >> (4 * (row & 3))) & 15);
+}
 
 // 16 bytes per lane from global memory straight into LDS at lds_base + 16 *
 // lane (global_load_lds_dwordx4; M0 holds the LDS base and is restored).
@@ -100,11 +108,11 @@ __device__ __forceinline__ void issue_stage(unsigned char* stage, const uint16_t
   for (int j = 0; j < 4; ++j) {
     const int row = 16 * wave + 4 * j + (lane >> 4);
     const int grow = min(k0 + row, N - 1);
-    const int chunk = swz(row, pos);
-    const size_t off = (size_t)grow * kHeadDim + 8 * chunk;
+    const size_t roff = (size_t)grow * kHeadDim;
     const uint32_t dst = base + (uint32_t)((16 * wave + 4 * j) * kRowBytes);
-    copy16_to_lds(kh + off, __builtin_amdgcn_readfirstlane(dst));
-    copy16_to_lds(vh + off, __builtin_amdgcn_readfirstlane(dst + kTileBytes));
+    copy16_to_lds(kh + roff + 8 * swz(row, pos), __builtin_amdgcn_readfirstlane(dst));
+    copy16_to_lds(vh + roff + 8 * swz_v(row, pos),
+                  __builtin_amdgcn_readfirstlane(dst + kTileBytes));
   }
 }
 
@@ -125,7 +133,7 @@ __device__ __forceinline__ bf16x8 read_vt(const unsigned char* stage, int dt, in
 #pragma unroll
   for (int a = 0; a < 2; ++a) {
     const int row = 16 * t + 8 * a + 4 * (g >> 1) + (i >> 2);
-    const unsigned char* p = vt + row * kRowBytes + 16 * swz(row, d >> 3) + 2 * (d & 7);
+    const unsigned char* p = vt + row * kRowBytes + 16 * swz_v(row, d >> 3) + 2 * (d & 7);
     r[a] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)p);
   }
   const uint2 lo = __builtin_bit_cast(uint2, r[0]), hi = __builtin_bit_cast(uint2, r[1]);
