@@ -74,7 +74,8 @@ struct ProbeShape {
 };
 
 // Workspace layout of the probe: Q representation (binary64) then K
-// representation (bf16 bits), both 256-byte aligned.
+// representation (fp32, blocks padded to a multiple of 64), both 256-byte
+// aligned.
 size_t probe_qrep_bytes(const ProbeShape& s);
 size_t probe_krep_bytes(const ProbeShape& s);
 // Largest C_B the scores kernel supports (LDS bound); 0 if none.

@@ -7,7 +7,10 @@
 //                 writes Q_max/Q_min per segment in binary64 (so the scores
 //                 kernel can read them as uniform scalar operands) and
 //                 K_max/K_min per key block in fp32 (exact: pooled values are
-//                 input values; one convert to binary64 per use).
+//                 input values; one convert to binary64 per use), tiled by 64
+//                 blocks: [head][j / 64][max|min][d / 4][j % 64][4], so that
+//                 the scores kernel's loads (lane = block, 4 dims per load)
+//                 read 1 KB contiguous per wave instruction.
 //  scores_kernel  one workgroup per (b, KV head, segment, chunk of query
 //                 heads).  Each lane owns one visible key block and forms the
 //                 4 logits of every query head of the chunk in binary64 FMA
@@ -26,6 +29,19 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWavesPerBlock = kThreads / kWave;
+
+// K representation tile: 64 blocks x (max, min) x 128 dims in fp32.
+constexpr int kKTileBlocks = 64;
+constexpr int kKTileFloats = kKTileBlocks * 2 * kHeadDim;
+__host__ __device__ inline int padded_blocks(int CB) {
+  return (CB + kKTileBlocks - 1) / kKTileBlocks * kKTileBlocks;
+}
+// Offset (floats) of block j's value for dims 4 dq .. 4 dq + 3 of part m
+// (0 = max, 1 = min) inside one head's K representation.
+__host__ __device__ inline size_t krep_offset(int j, int m, int dq) {
+  return (size_t)(j / kKTileBlocks) * kKTileFloats +
+         (size_t)((m * (kHeadDim / 4) + dq) * kKTileBlocks + j % kKTileBlocks) * 4;
+}
 
 __global__ __launch_bounds__(kThreads) void pool_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, int B, int Hq, int Hkv,
@@ -96,11 +112,11 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(
       *(double2*)(out + kHeadDim + e) = make_double2((double)mn[e], (double)mn[e + 1]);
     }
   } else {
-    float* out = krep + ((size_t)head * CB + grp) * 2 * kHeadDim + 8 * c;
-    *(float4*)out = make_float4(mx[0], mx[1], mx[2], mx[3]);
-    *(float4*)(out + 4) = make_float4(mx[4], mx[5], mx[6], mx[7]);
-    *(float4*)(out + kHeadDim) = make_float4(mn[0], mn[1], mn[2], mn[3]);
-    *(float4*)(out + kHeadDim + 4) = make_float4(mn[4], mn[5], mn[6], mn[7]);
+    float* out = krep + (size_t)head * padded_blocks(CB) * 2 * kHeadDim;
+    *(float4*)(out + krep_offset(grp, 0, 2 * c)) = make_float4(mx[0], mx[1], mx[2], mx[3]);
+    *(float4*)(out + krep_offset(grp, 0, 2 * c + 1)) = make_float4(mx[4], mx[5], mx[6], mx[7]);
+    *(float4*)(out + krep_offset(grp, 1, 2 * c)) = make_float4(mn[0], mn[1], mn[2], mn[3]);
+    *(float4*)(out + krep_offset(grp, 1, 2 * c + 1)) = make_float4(mn[4], mn[5], mn[6], mn[7]);
   }
 }
 
@@ -169,13 +185,13 @@ __global__ __launch_bounds__(NT) void scores_kernel(
 #pragma unroll
   for (int hh = 0; hh < HPW; ++hh)
     qv[hh] = qrep + ((size_t)(b * Hq + h0 + min(hh, nh - 1)) * CS + s) * 2 * kHeadDim;
-  const float* kb = krep + (size_t)(b * Hkv + g) * CB * 2 * kHeadDim;
+  const float* kb = krep + (size_t)(b * Hkv + g) * padded_blocks(CB) * 2 * kHeadDim;
 
   // Phase 1: exact logits, one key block per lane.
   for (int j0 = wave * kWave; j0 < nvis; j0 += NT) {
     const int j = j0 + lane;
     const bool valid = j < nvis;
-    const float* kr = kb + (size_t)(valid ? j : nvis - 1) * 2 * kHeadDim;
+    const float* kr = kb + krep_offset(valid ? j : nvis - 1, 0, 0);
     double acc[HPW][4];
 #pragma unroll
     for (int hh = 0; hh < HPW; ++hh)
@@ -184,10 +200,12 @@ __global__ __launch_bounds__(NT) void scores_kernel(
 #pragma unroll 2
     for (int d0 = 0; d0 < kHeadDim; d0 += 8) {
       double kx[8], kn[8];
-      widen4(*(const float4*)(kr + d0), kx);
-      widen4(*(const float4*)(kr + d0 + 4), kx + 4);
-      widen4(*(const float4*)(kr + kHeadDim + d0), kn);
-      widen4(*(const float4*)(kr + kHeadDim + d0 + 4), kn + 4);
+      constexpr int kDq = 4 * kKTileBlocks;             // floats between dim quads
+      constexpr int kMin = (kHeadDim / 4) * kDq;        // max part -> min part
+      widen4(*(const float4*)(kr + (d0 / 4) * kDq), kx);
+      widen4(*(const float4*)(kr + (d0 / 4 + 1) * kDq), kx + 4);
+      widen4(*(const float4*)(kr + kMin + (d0 / 4) * kDq), kn);
+      widen4(*(const float4*)(kr + kMin + (d0 / 4 + 1) * kDq), kn + 4);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
 #pragma unroll
@@ -351,7 +369,7 @@ size_t probe_qrep_bytes(const ProbeShape& s) {
   return align_up((size_t)s.B * s.Hq * s.CS * 2 * kHeadDim * sizeof(double));
 }
 size_t probe_krep_bytes(const ProbeShape& s) {
-  return align_up((size_t)s.B * s.Hkv * s.CB * 2 * kHeadDim * sizeof(float));
+  return align_up((size_t)s.B * s.Hkv * padded_blocks(s.CB) * 2 * kHeadDim * sizeof(float));
 }
 
 bool probe_supported(const ProbeShape& s) {
