@@ -9,10 +9,14 @@
 //                 recurrence is written, so the result is bit-identical to any
 //                 other IEEE evaluation in that order.
 //  topk_kernel    one wave per (b, h, s) row: the row's past-block scores sit
-//                 in registers as order-preserving 32-bit keys; the k-th
-//                 largest key is found bit by bit with ballot counts, ties at
-//                 the threshold keep the highest block indices, and the chosen
-//                 blocks plus the segment's own blocks are written ascending.
+//                 in registers as order-preserving 32-bit keys.  The k-th
+//                 largest key T is found by radix selection: an 11-bit
+//                 histogram (in LDS) of the bits below the keys' common prefix
+//                 picks T's bucket; the keys of that bucket (usually few) are
+//                 compacted to one per lane and T's remaining bits are
+//                 resolved there with one ballot per bit.  Ties at T keep the
+//                 highest block indices; the chosen blocks plus the segment's
+//                 own blocks are written ascending.
 #include "ei_internal.h"
 
 #include <math.h>
@@ -97,12 +101,28 @@ __device__ __forceinline__ uint32_t score_key(float v) {
   return k + 1u;   // finite/inf keys are <= 0xff800000, so no wrap
 }
 
+constexpr int kWavesPerGroup = kThreads / kWave;
+constexpr int kHistBits = 11;
+constexpr int kHistBins = 1 << kHistBits;
+
+// Order within one wave between its LDS writes and the reads of other lanes.
+__device__ __forceinline__ void wave_lds_fence() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 template <int SLOTS>
 __global__ __launch_bounds__(kThreads) void topk_kernel(
     const float* __restrict__ log_scores, const int32_t* __restrict__ kblocks, int64_t rows,
     int CS, int CB, int r, int kmax, int32_t* __restrict__ idx, int32_t* __restrict__ cnt) {
-  const int64_t row = (int64_t)blockIdx.x * (kThreads / kWave) + (threadIdx.x >> 6);
-  if (row >= rows) return;
+  // per-wave scratch: bucket counts and the compacted keys of T's bucket
+  __shared__ __attribute__((aligned(16))) uint32_t hist_all[kWavesPerGroup][kHistBins];
+  __shared__ uint32_t cand_all[kWavesPerGroup][kWave];
+  const int wv = threadIdx.x >> 6;
+  const int64_t row = (int64_t)blockIdx.x * kWavesPerGroup + wv;
+  if (row >= rows) return;   // no workgroup barriers below
+  uint32_t* hist = hist_all[wv];
+  uint32_t* cand = cand_all[wv];
   const int lane = threadIdx.x & (kWave - 1);
   const int s = (int)(row % CS);
   const int npast = s * r;
@@ -130,38 +150,123 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
     }
     kmx = wave_max_u32(kmx);
     kmn = wave_min_u32(kmn);
-    // Every valid key shares the high bits where kmx and kmn agree; so does
-    // the k-th largest.  Resolve the remaining bits from the top.
+    // T = the kk-th largest key; gt / eq = keys above / equal to T.
     uint32_t T;
+    int gt = -1, eq = -1;
     if (kmx == kmn) {
       T = kmx;
+      gt = 0;
+      eq = npast;
     } else {
+      // Valid keys share the bits above `top`; bucket them by the next
+      // (up to) 11 bits.
       const int top = 31 - __clz(kmx ^ kmn);
-      T = kmx & ~((top == 31) ? 0xffffffffu : ((2u << top) - 1u));
-      for (int bit = top; bit >= 0; --bit) {
-        const uint32_t cand = T | (1u << bit);
-        int c = 0;
+      const uint32_t prefix = kmx & ~((top == 31) ? 0xffffffffu : ((2u << top) - 1u));
+      const int shift = max(top - (kHistBits - 1), 0);
+      const uint32_t dmask = (2u << (top - shift)) - 1u;
+      for (int i = lane; i < kHistBins / 4; i += kWave) ((uint4*)hist)[i] = make_uint4(0, 0, 0, 0);
+      wave_lds_fence();
 #pragma unroll
-        for (int sl = 0; sl < SLOTS; ++sl)
-          if (sl < nsl) c += popc64(__ballot(key[sl] >= cand));
-        if (c >= kk) T = cand;
+      for (int sl = 0; sl < SLOTS; ++sl)
+        if (sl < nsl && key[sl]) atomicAdd(&hist[(key[sl] >> shift) & dmask], 1u);
+      wave_lds_fence();
+      // Lane l owns buckets 32 l .. 32 l + 31; find the bucket holding T from
+      // the top: the largest d with (keys in buckets >= d) >= kk.
+      uint32_t cl[32];
+#pragma unroll
+      for (int qd = 0; qd < 8; ++qd) {
+        const uint4 w = ((const uint4*)(hist + 32 * lane))[qd];
+        cl[4 * qd] = w.x;
+        cl[4 * qd + 1] = w.y;
+        cl[4 * qd + 2] = w.z;
+        cl[4 * qd + 3] = w.w;
+      }
+      uint32_t S = 0;
+#pragma unroll
+      for (int d = 0; d < 32; ++d) S += cl[d];
+      uint32_t pre = S;   // inclusive prefix over lanes
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) {
+        const uint32_t t = __shfl_up(pre, o);
+        if (lane >= o) pre += t;
+      }
+      const uint32_t total = __shfl(pre, kWave - 1);
+      const uint32_t suf = total - pre + S;   // keys in buckets of lanes >= lane
+      const uint64_t okm = __ballot(suf >= (uint32_t)kk);
+      const int ls = 63 - __clzll(okm);     // okm != 0: total = npast > kk
+      int dstar = 0;
+      uint32_t above = 0;
+      if (lane == ls) {
+        uint32_t acc = suf - S;
+        for (int d = 31; d >= 0; --d) {
+          const uint32_t nacc = acc + cl[d];
+          if (nacc >= (uint32_t)kk) {
+            dstar = 32 * lane + d;
+            above = acc;
+            break;
+          }
+          acc = nacc;
+        }
+      }
+      dstar = __shfl(dstar, ls);
+      above = __shfl(above, ls);
+      const uint32_t nb = hist[dstar];
+      T = prefix | ((uint32_t)dstar << shift);
+      if (shift == 0) {
+        gt = (int)above;
+        eq = (int)nb;
+      } else if (nb <= (uint32_t)kWave) {
+        // compact the bucket's keys, one per lane, and resolve the low bits
+        int cp = 0;
+#pragma unroll
+        for (int sl = 0; sl < SLOTS; ++sl) {
+          if (sl >= nsl) break;
+          const bool in = key[sl] != 0u && ((key[sl] >> shift) & dmask) == (uint32_t)dstar;
+          const uint64_t m = __ballot(in);
+          if (in) cand[cp + popc64(m & lt_mask)] = key[sl];
+          cp += popc64(m);
+        }
+        wave_lds_fence();
+        const uint32_t ck = lane < (int)nb ? cand[lane] : 0u;
+        for (int bit = shift - 1; bit >= 0; --bit) {
+          const uint32_t c = T | (1u << bit);
+          if ((int)above + popc64(__ballot(ck >= c)) >= kk) T = c;
+        }
+        gt = (int)above + popc64(__ballot(ck > T));
+        eq = popc64(__ballot(ck == T));
+      } else {
+        // large bucket (many equal high bits): resolve over all slots
+        for (int bit = shift - 1; bit >= 0; --bit) {
+          const uint32_t c = T | (1u << bit);
+          int n = 0;
+#pragma unroll
+          for (int sl = 0; sl < SLOTS; ++sl)
+            if (sl < nsl) n += popc64(__ballot(key[sl] >= c));
+          if (n >= kk) T = c;
+        }
       }
     }
-    int gt = 0;
+    if (gt < 0) {
+      gt = 0;
+      eq = 0;
 #pragma unroll
-    for (int sl = 0; sl < SLOTS; ++sl)
-      if (sl < nsl) gt += popc64(__ballot(key[sl] > T));
-    const int need = kk - gt;   // >= 1 keys equal to T, highest indices first
+      for (int sl = 0; sl < SLOTS; ++sl)
+        if (sl < nsl) {
+          gt += popc64(__ballot(key[sl] > T));
+          eq += popc64(__ballot(key[sl] == T));
+        }
+    }
+    const int need = kk - gt;   // 1 .. eq keys equal to T, highest indices first
     int J = 0;
-    {
+    if (need < eq) {
       const int top = 31 - __clz(max(npast - 1, 1));
       for (int bit = top; bit >= 0; --bit) {
-        const int cand = J | (1 << bit);
-        int c = 0;
+        const int c = J | (1 << bit);
+        int n = 0;
 #pragma unroll
         for (int sl = 0; sl < SLOTS; ++sl)
-          if (sl < nsl) c += popc64(__ballot(key[sl] == T && sl * kWave + lane >= cand));
-        if (c >= need) J = cand;
+          if (sl < nsl) n += popc64(__ballot(key[sl] == T && sl * kWave + lane >= c));
+        if (n >= need) J = c;
       }
     }
 #pragma unroll

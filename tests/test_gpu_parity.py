@@ -209,6 +209,47 @@ def test_malformed_block_list_is_safe():
     assert np.abs(got - ref).max() <= ATTN_ABS
 
 
+def _crafted_scores(CS, CB, Hq, seed=5):
+    """Score rows that reach every branch of the GPU selector: exact ties,
+    NaN / +-inf / +-0, rows of one value, a bucket of far more than 64 keys
+    (two clusters that differ in one high mantissa bit), keys that differ
+    only in their low 10 bits, and plain random rows."""
+    rng = np.random.default_rng(seed)
+    ls = np.empty((1, Hq, CS, CB), np.float32)
+    shape = (CS, CB)
+    ls[0, 0] = rng.choice(np.array([-1.5, -2.25, -3.0, -0.0, 0.0], np.float32), shape)
+    x = rng.standard_normal(shape).astype(np.float32)
+    u = rng.random(shape)
+    x[u < 0.1] = np.nan
+    x[(u >= 0.1) & (u < 0.15)] = -np.inf
+    x[(u >= 0.15) & (u < 0.17)] = np.inf
+    ls[0, 1] = x
+    ls[0, 2] = -4.0
+    bits = (0x3F800000 + rng.integers(0, 2, shape) * (1 << 20)
+            + rng.integers(0, 512, shape)).astype(np.uint32)
+    ls[0, 3] = bits.view(np.float32)
+    ls[0, 4] = (0x3F800000 + rng.integers(0, 1024, shape)).astype(np.uint32).view(np.float32)
+    ls[0, 5] = rng.standard_normal(shape).astype(np.float32)
+    en = rng.uniform(0.5, 1.5, (1, Hq, CS)).astype(np.float32)
+    en[0, 2] = 0.0                                               # a rigid head
+    return ls, en
+
+
+def test_select_crafted_scores():
+    """Selection is bit-exact against the oracle on crafted score rows."""
+    N, Ls, Lb, Hq = 32768, 128, 64, 6
+    CS, CB = N // Ls, N // Lb
+    ls, en = _crafted_scores(CS, CB, Hq)
+    for bh, mult in ((2048, 3), (64, 3), (8192, 3)):
+        sel = eb.select_blocks(torch.from_numpy(ls).cuda(), torch.from_numpy(en).cuda(), N, Ls,
+                               Lb, 1e-5, 0.5, 0.4, bh, mult, n_kv_heads=Hq)
+        torch.cuda.synchronize()
+        g = {kk: t.cpu().numpy() for kk, t in sel.items()}
+        ref = oracle.select(ls, en, N, Ls, Lb, 1e-5, 0.5, 0.4, bh, mult)
+        for name in ("rigid", "budget", "cnt", "idx"):
+            np.testing.assert_array_equal(g[name], ref[name], err_msg=f"{name} B_h={bh}")
+
+
 def _sample_rows(w, n_seg=48, seed=0):
     rng = np.random.default_rng(seed)
     segs = np.unique(np.concatenate([[0, 1, w.CS - 1], rng.integers(0, w.CS, n_seg)]))
