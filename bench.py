@@ -85,7 +85,7 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--dense-reps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-budget-s", type=float, default=20.0)
+    ap.add_argument("--cpu-budget-s", type=float, default=15.0)
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run one device-to-device copy of this size, so that a "
                          "rocprofv3 --pmc run can scale FETCH_SIZE / WRITE_SIZE by it")
@@ -256,12 +256,23 @@ def cpu_baseline(w, bufs, cnt, idx, pairs, budget_s):
     rng = np.random.default_rng(123)
     r_ = w.Ls // w.Lb
     nvis = np.minimum((np.arange(w.CS) + 1) * r_, w.CB)
-    # probe: a spread of segments x all heads
-    segs = np.linspace(0, w.CS - 1, 8).astype(int)
-    rows = np.array([[0, h, s] for s in segs for h in range(w.Hq)], np.int32)
-    t0 = time.perf_counter()
-    oracle.probe(w.q, w.k, w.Ls, w.Lb, w.probe_scale, rows=rows)
-    t_probe = time.perf_counter() - t0
+    # Each sample is sized from a short calibration run so that probe and
+    # attention take about 0.35 and 0.5 of the budget.
+    def probe_rows(n_seg):
+        segs = np.unique(np.linspace(0, w.CS - 1, n_seg).astype(int))
+        return np.array([[0, h, s] for s in segs for h in range(w.Hq)], np.int32)
+
+    def time_probe(rows):
+        t0 = time.perf_counter()
+        oracle.probe(w.q, w.k, w.Ls, w.Lb, w.probe_scale, rows=rows)
+        return time.perf_counter() - t0
+
+    rows = probe_rows(8)
+    t_probe = time_probe(rows)
+    n_seg = int(min(w.CS, max(8, 8 * 0.35 * budget_s / max(t_probe, 1e-3))))
+    if n_seg > 8:
+        rows = probe_rows(n_seg)
+        t_probe = time_probe(rows)
     probe_full = t_probe * (w.B * w.Hq * nvis.sum()) / nvis[rows[:, 2]].sum()
     # selection: the whole layer on the GPU's fp32 scores
     ls = bufs["log_scores"].cpu().numpy()
@@ -269,30 +280,39 @@ def cpu_baseline(w, bufs, cnt, idx, pairs, budget_s):
     t0 = time.perf_counter()
     oracle.select(ls, en, w.N, w.Ls, w.Lb, w.e_t, w.alpha, w.delta_t, w.base_budget, w.mult)
     t_sel = time.perf_counter() - t0
+
     # attention: query rows drawn uniformly, extrapolated by causal pairs
-    n = 16
-    qrows = np.stack([np.zeros(n, int), rng.integers(0, w.Hq, n), rng.integers(0, w.N, n)],
-                     axis=1).astype(np.int32)
-    while True:
+    def query_rows(n):
+        return np.stack([np.zeros(n, int), rng.integers(0, w.Hq, n), rng.integers(0, w.N, n)],
+                        axis=1).astype(np.int32)
+
+    def time_attention(qrows):
         t0 = time.perf_counter()
         oracle.attention(w.q, w.k, w.v, qrows, w.softmax_scale, True, idx, cnt, w.Ls, w.Lb)
-        t_att = time.perf_counter() - t0
-        if t_att > 0.2 * budget_s or n >= 4096:
-            break
-        n *= 2
-        qrows = np.stack([np.zeros(n, int), rng.integers(0, w.Hq, n), rng.integers(0, w.N, n)],
-                         axis=1).astype(np.int32)
+        return time.perf_counter() - t0
+
+    qrows = query_rows(1024)
+    t_att = time_attention(qrows)
+    n = int(min(1 << 19, max(1024, 1024 * 0.5 * budget_s / max(t_att, 1e-3))))
+    if n > 1024:
+        qrows = query_rows(n)
+        t_att = time_attention(qrows)
     sample_pairs = 0
-    for b, h, i in qrows:
-        s = i // w.Ls
-        for blk in idx[b, h, s, : cnt[b, h, s]]:
-            k0, k1 = blk * w.Lb, min((blk + 1) * w.Lb, w.N)
-            sample_pairs += max(0, min(k1, i + 1) - k0)
+    for c0 in range(0, len(qrows), 1 << 15):
+        qb = qrows[c0:c0 + (1 << 15)]
+        seg = qb[:, 2] // w.Ls
+        blk = idx[qb[:, 0], qb[:, 1], seg].astype(np.int64)               # [n, kmax]
+        live = np.arange(blk.shape[1])[None, :] < cnt[qb[:, 0], qb[:, 1], seg][:, None]
+        k0 = blk * w.Lb
+        k1 = np.minimum(k0 + w.Lb, w.N)
+        span = np.minimum(k1, qb[:, 2:3].astype(np.int64) + 1) - k0
+        sample_pairs += int(np.where(live, np.maximum(span, 0), 0).sum())
     att_full = t_att * pairs / max(sample_pairs, 1)
     total_s = probe_full + t_sel + att_full
     return {"value": round(total_s * 1e3, 1), "unit": "ms/layer", "cores": cores,
             "kind": "oracle",
-            "sample": (f"probe: {len(rows)} (head, segment) rows at 8 positions, {t_probe:.2f}s, "
+            "sample": (f"probe: {len(rows)} (head, segment) rows at {len(rows) // w.Hq} segment "
+                       f"positions, {t_probe:.2f}s, "
                        f"scaled by visible blocks; select: whole layer, {t_sel:.2f}s; attention: "
                        f"{len(qrows)} random query rows, {t_att:.2f}s, scaled by causal pairs"),
             "stages_s": {"probe": round(probe_full, 2), "select": round(t_sel, 2),
