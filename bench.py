@@ -26,6 +26,7 @@ PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 ATTN_SOURCES = ["paper_2606_09508_amd/csrc/ei_attn.hip", "paper_2606_09508_amd/csrc/ei_internal.h"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_sparse_llama8b_128k_traffic.txt")
+SQ_FILE = os.path.join(ROOT, "profiles", "attn_sparse_llama8b_128k_sq_counters.txt")
 
 
 def sources_hash(paths) -> str:
@@ -36,22 +37,46 @@ def sources_hash(paths) -> str:
     return h.hexdigest()[:16]
 
 
-def read_traffic():
-    """HBM bytes per launch of the sparse attention kernel from the committed
-    rocprofv3 counter summary, if it was taken on the current kernel source."""
-    if not os.path.exists(TRAFFIC_FILE):
+def read_counter_file(path, key):
+    """A value from a committed rocprofv3 counter summary of the sparse
+    attention kernel, if the summary was taken on the current kernel source."""
+    if not os.path.exists(path):
         return None
     kv = {}
-    for line in open(TRAFFIC_FILE):
+    for line in open(path):
         if ":" in line and not line.startswith("#"):
             a, b = line.split(":", 1)
             kv[a.strip()] = b.strip()
     if kv.get("attn_source_hash") != sources_hash(ATTN_SOURCES):
         return None
     try:
-        return float(kv["hbm_bytes_per_launch"])
+        return float(kv[key])
     except (KeyError, ValueError):
         return None
+
+
+def read_traffic():
+    """HBM bytes per launch of the sparse attention kernel."""
+    return read_counter_file(TRAFFIC_FILE, "hbm_bytes_per_launch")
+
+
+def tile_flops(cnt: np.ndarray, N: int, Ls: int, Lb: int) -> float:
+    """MFMA flops the sparse kernel issues: per listed 64-key sub-block, every
+    32-row wave of the 128-row tile that has a query at or after the
+    sub-block's first key computes S and P V over the full 32 x 64 tile."""
+    B, Hq, CS = cnt.shape
+    r = Ls // Lb
+    per_wave = 2.0 * 2 * 32 * 64 * 128
+    total = 0.0
+    for s in range(CS):
+        q0 = s * Ls
+        waves = [w for w in range(Ls // 32) if q0 + 32 * w < N]
+        own_blocks = range(s * r, min((s + 1) * r, -(-N // Lb)))
+        own_subs = [(j * Lb + 64 * t) for j in own_blocks for t in range(Lb // 64)]
+        own_cost = sum(sum(1 for w in waves if k0 <= q0 + 32 * w + 31) for k0 in own_subs)
+        n_past = (cnt[:, :, s].astype(np.int64) - len(own_blocks)).clip(min=0).sum()
+        total += per_wave * (float(n_past) * (Lb // 64) * len(waves) + own_cost * B * Hq)
+    return total
 
 
 def causal_pairs(cnt: np.ndarray, idx: np.ndarray, N: int, Ls: int, Lb: int) -> int:
@@ -165,6 +190,7 @@ def main():
     st = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
                    for e in evs])
     probe_ms, select_ms, sparse_ms = [float(x) for x in st.mean(axis=0)]
+    pct = np.percentile(st, [10, 50, 90], axis=0)
 
     # dense baseline on the same inputs
     od = torch.empty_like(q)
@@ -187,6 +213,7 @@ def main():
     dense_pairs = w.B * w.Hq * w.N * (w.N + 1) // 2
     dense_flops = 4.0 * w.D * dense_pairs
     sparse_tflops = sparse_flops / (sparse_ms * 1e-3) / 1e12
+    sparse_tile_tflops = tile_flops(cnt, w.N, w.Ls, w.Lb) / (sparse_ms * 1e-3) / 1e12
     dense_tflops = dense_flops / (dense_ms * 1e-3) / 1e12
 
     r_ = w.Ls // w.Lb
@@ -230,8 +257,12 @@ def main():
                    "parallelism": "single GPU"},
         "stages_ms": {"probe": round(probe_ms, 4), "select": round(select_ms, 4),
                       "sparse_attn": round(sparse_ms, 4)},
+        "stages_ms_p10_p50_p90": {name: [round(float(x), 4) for x in pct[:, i]]
+                                  for i, name in enumerate(("probe", "select", "sparse_attn"))},
         "mfma_util": round(sparse_tflops / PEAK_BF16_TFLOPS, 4),
         "sparse_attn_tflops": round(sparse_tflops, 2),
+        "sparse_attn_tile_tflops": round(sparse_tile_tflops, 2),
+        "mfma_busy_counter": read_counter_file(SQ_FILE, "mfma_busy_fraction"),
         "dense_ms": round(dense_ms, 3),
         "dense_tflops": round(dense_tflops, 2),
         "speedup_vs_dense": round(dense_ms / total_ms, 3),
