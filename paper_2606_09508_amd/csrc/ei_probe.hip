@@ -15,8 +15,11 @@
 //                 heads).  Each lane owns one visible key block and forms the
 //                 4 logits of every query head of the chunk in binary64 FMA
 //                 (products of bf16 values are exact, so the logits equal the
-//                 plain definition's); it keeps fp32 offsets from a per-wave
-//                 reference in LDS; then one wave per logit row finds the
+//                 plain definition's); the query representation is staged in
+//                 LDS and read with broadcast loads (in-order completion, so
+//                 they pipeline, unlike scalar loads); the kernel keeps fp32
+//                 offsets from a per-wave reference in LDS; then one wave per
+//                 logit row finds the
 //                 row's maximum, argmax and log-sum-exp, and the waves of
 //                 each head evaluate A = max((S1+S2)/2, (S3+S4)/2) and
 //                 H = -sum A ln A in log space (fp32 terms, fp64 sums).
@@ -163,7 +166,8 @@ __global__ __launch_bounds__(NT) void scores_kernel(
   extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
   RowStats* stats = (RowStats*)smem_raw;                        // [R]
   double* hpart = (double*)(smem_raw + sizeof(RowStats) * R);   // [W]
-  float* ys = (float*)(hpart + W);                              // [R][ldy] offsets x - ref
+  double* qs = hpart + W;                                       // [HPW][128][max, min]
+  float* ys = (float*)(qs + HPW * 2 * kHeadDim);                // [R][ldy] offsets x - ref
   float* refs = ys + R * ldy;                                   // [R][ldy / 64] references
   const int nref = ldy >> 6;
 
@@ -181,10 +185,12 @@ __global__ __launch_bounds__(NT) void scores_kernel(
   const int nvis = min((s + 1) * r, CB);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
 
-  const double* qv[HPW];
-#pragma unroll
-  for (int hh = 0; hh < HPW; ++hh)
-    qv[hh] = qrep + ((size_t)(b * Hq + h0 + min(hh, nh - 1)) * CS + s) * 2 * kHeadDim;
+  for (int t = threadIdx.x; t < HPW * 2 * kHeadDim; t += NT) {
+    const int hh = t / (2 * kHeadDim), m = (t / kHeadDim) & 1, d = t % kHeadDim;
+    const double* qv = qrep + ((size_t)(b * Hq + h0 + min(hh, nh - 1)) * CS + s) * 2 * kHeadDim;
+    qs[(hh * kHeadDim + d) * 2 + m] = qv[m * kHeadDim + d];
+  }
+  __syncthreads();
   const float* kb = krep + (size_t)(b * Hkv + g) * padded_blocks(CB) * 2 * kHeadDim;
 
   // Phase 1: exact logits, one key block per lane.
@@ -210,7 +216,8 @@ __global__ __launch_bounds__(NT) void scores_kernel(
       for (int e = 0; e < 8; ++e) {
 #pragma unroll
         for (int hh = 0; hh < HPW; ++hh) {
-          const double qa = qv[hh][d0 + e], qb = qv[hh][kHeadDim + d0 + e];
+          const double2 qq = *(const double2*)(qs + (hh * kHeadDim + d0 + e) * 2);
+          const double qa = qq.x, qb = qq.y;
           acc[hh][0] = fma(qa, kx[e], acc[hh][0]);   // S1: Q_max . K_max
           acc[hh][1] = fma(qa, kn[e], acc[hh][1]);   // S2: Q_max . K_min
           acc[hh][2] = fma(qb, kx[e], acc[hh][2]);   // S3: Q_min . K_max
@@ -306,7 +313,8 @@ constexpr size_t kMaxLds = 160 * 1024;
 
 size_t scores_lds_bytes(int hpw, int nt, int ldy) {
   const size_t R = 4 * (size_t)hpw;
-  return sizeof(RowStats) * R + sizeof(double) * (size_t)(nt / kWave) + R * (size_t)ldy * 4 +
+  return sizeof(RowStats) * R + sizeof(double) * (size_t)(nt / kWave) +
+         sizeof(double) * (size_t)hpw * 2 * kHeadDim + R * (size_t)ldy * 4 +
          R * (size_t)(ldy / 64) * 4;
 }
 
