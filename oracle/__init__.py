@@ -48,6 +48,15 @@ def lib():
         L.orc_select.argtypes = [_f32p, _f32p, _c_int, _c_int, _c_int, _c_int, _c_int, _c_flt,
                                  _c_dbl, _c_dbl, _c_i32, _c_i32, _c_i32, _u8p, _i32p, _i32p,
                                  _i32p]
+        L.orc_select_mode.restype = _c_int
+        L.orc_select_mode.argtypes = [_f32p, _f32p, _c_int, _c_int, _c_int, _c_int, _c_int,
+                                      _c_int, _c_int, _c_flt, _c_dbl, _c_dbl, _c_i32, _c_i32,
+                                      _c_i32, _u8p, _i32p, _i32p, _i32p]
+        L.orc_budget_segment.restype = _c_int
+        L.orc_budget_segment.argtypes = [_f32p, _c_i64, _c_flt, _c_dbl, _c_dbl, _c_i32, _c_i32,
+                                         _f64p]
+        L.orc_group_entropy.restype = None
+        L.orc_group_entropy.argtypes = [_f32p, _c_i64, _c_int, _f32p]
         L.orc_attention.restype = _c_int
         L.orc_attention.argtypes = [_u16p, _u16p, _u16p, _c_int, _c_int, _c_int, _c_int, _c_int,
                                     _c_int, _c_int, _c_dbl, _c_int, ctypes.c_void_p,
@@ -123,15 +132,37 @@ def budget(e, e_t=1e-5, alpha=0.5, delta_t=0.4, base_budget=2048, mult=3):
     return bool(rigid), B[: e.shape[0]]
 
 
+def budget_segment(e, e_t=1e-5, alpha=0.5, delta_t=0.4, base_budget=2048, mult=3):
+    """The per-segment rigid rule on one head's entropies -> (all rigid, B)."""
+    e = np.ascontiguousarray(np.asarray(e, np.float32))
+    B = np.empty((max(1, e.shape[0]),), np.float64)
+    rigid = lib().orc_budget_segment(e, e.shape[0], float(e_t), float(alpha), float(delta_t),
+                                     int(base_budget), int(mult), B)
+    return bool(rigid), B[: e.shape[0]]
+
+
+def group_entropy(e_group):
+    """[G, C_S] entropies of one GQA group -> [C_S] binary32 group means."""
+    e = np.ascontiguousarray(np.asarray(e_group, np.float32))
+    out = np.empty((e.shape[1],), np.float32)
+    lib().orc_group_entropy(e, e.shape[1], e.shape[0], out)
+    return out
+
+
+# classification modes of select()
+CLASSIFY_HEAD, CLASSIFY_GQA_GROUP, CLASSIFY_SEGMENT = 0, 1, 2
+
+
 def kmax(Ls: int, Lb: int, base_budget: int, mult: int) -> int:
     return (mult * base_budget) // Lb + Ls // Lb
 
 
 def select(log_scores, entropy, N: int, Ls: int, Lb: int, e_t=1e-5, alpha=0.5, delta_t=0.4,
-           base_budget=2048, mult=3, kmax_=None):
+           base_budget=2048, mult=3, kmax_=None, mode=CLASSIFY_HEAD, n_kv_heads=None):
     """Classification, budgets and top-k selection from binary32 inputs.
 
-    log_scores [B, Hq, C_S, C_B] fp32, entropy [B, Hq, C_S] fp32.
+    log_scores [B, Hq, C_S, C_B] fp32, entropy [B, Hq, C_S] fp32.  mode: one
+    of the CLASSIFY_* constants (n_kv_heads is needed for the GQA-group mode).
     Returns dict(rigid [B,Hq] u8, budget [B,Hq,C_S] i32, idx [B,Hq,C_S,kmax] i32,
     cnt [B,Hq,C_S] i32).
     """
@@ -143,8 +174,10 @@ def select(log_scores, entropy, N: int, Ls: int, Lb: int, e_t=1e-5, alpha=0.5, d
     bud = np.empty((B, Hq, CS), np.int32)
     idx = np.empty((B, Hq, CS, km), np.int32)
     cnt = np.empty((B, Hq, CS), np.int32)
-    _check(lib().orc_select(ls, en, B, Hq, N, Ls, Lb, float(e_t), float(alpha), float(delta_t),
-                            int(base_budget), int(mult), km, rigid, bud, idx, cnt), "select")
+    hkv = Hq if n_kv_heads is None else int(n_kv_heads)
+    _check(lib().orc_select_mode(ls, en, B, Hq, hkv, int(mode), N, Ls, Lb, float(e_t),
+                                 float(alpha), float(delta_t), int(base_budget), int(mult), km,
+                                 rigid, bud, idx, cnt), "select")
     return {"rigid": rigid, "budget": bud, "idx": idx, "cnt": cnt}
 
 

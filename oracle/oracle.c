@@ -48,6 +48,11 @@
 #define ORC_ERR_ARG (-1)
 #define ORC_ERR_MEM (-2)
 
+/* Classification modes of the selection (the method and two variants). */
+#define ORC_CLASSIFY_HEAD 0       /* Algorithm 3 per query head */
+#define ORC_CLASSIFY_GQA_GROUP 1  /* Algorithm 3 on the GQA-group mean entropy */
+#define ORC_CLASSIFY_SEGMENT 2    /* rigid rule applied per segment */
+
 static const double ORC_LN2 = 0.69314718055994530942;
 
 /* bf16 (the upper 16 bits of an IEEE binary32) to double; exact. */
@@ -270,6 +275,53 @@ int orc_budget(const float *e, int64_t cs, float e_t, double alpha,
   return 0;
 }
 
+/* Per-segment variant of the rigid rule (a reading of Algorithm 3 with the
+ * classification moved from the head to the segment): segment i with
+ * e_i < e_t takes the base budget B_0; every other segment i >= 1 follows
+ * Algorithm 3's update from the previous segment's budget.  Returns 1 iff
+ * every segment is rigid, in which case the result equals orc_budget's. */
+int orc_budget_segment(const float *e, int64_t cs, float e_t, double alpha,
+                       double delta_t, int32_t base_budget, int32_t mult,
+                       double *Bout) {
+  int rigid = 1;
+  for (int64_t i = 0; i < cs; ++i)
+    if (!(e[i] < e_t)) rigid = 0;
+  const double B0 = (double)base_budget;
+  const double cap = (double)mult * B0;
+  if (cs <= 0) return rigid;
+  Bout[0] = B0;
+  const double a = alpha * B0;
+  for (int64_t i = 1; i < cs; ++i) {
+    if (e[i] < e_t) {
+      Bout[i] = B0;
+      continue;
+    }
+    const double ep = (double)e[i - 1], ec = (double)e[i];
+    const double num = fabs(ec - ep);
+    const double ratio = (num == 0.0 && ep == 0.0) ? 0.0 : num / ep;
+    const double t = ratio - delta_t;
+    const double delta = a * t;
+    double Bn = Bout[i - 1] + delta;
+    if (!(Bn >= B0)) Bn = B0;
+    if (Bn > cap) Bn = cap;
+    Bout[i] = Bn;
+  }
+  return rigid;
+}
+
+/* GQA-group entropy (the per-group aggregation the paper plots as
+ * "Averaged"): the mean of the group's G query heads' entropies for each
+ * segment, summed in binary64 in head order, divided by G and rounded to
+ * binary32.  eg: [C_S] out; e_group: the group's first head's row of a
+ * [Hq][C_S] block. */
+void orc_group_entropy(const float *e_group, int64_t cs, int G, float *eg) {
+  for (int64_t i = 0; i < cs; ++i) {
+    double sum = 0.0;
+    for (int h = 0; h < G; ++h) sum += (double)e_group[(int64_t)h * cs + i];
+    eg[i] = (float)(sum / (double)G);
+  }
+}
+
 /* Orderable key of a binary32 ranking score: larger float -> larger key;
  * -0 == +0; NaN below -inf. */
 static uint32_t score_key(float v) {
@@ -299,35 +351,53 @@ static int cand_cmp(const void *pa, const void *pb) {
  * block_idx [B][Hq][C_S][kmax] ascending and -1 padded: the k_s past blocks of
  * largest score plus the segment's own blocks s r .. min((s+1) r, C_B) - 1,
  * block_cnt [B][Hq][C_S] = number of valid entries.
+ *
+ * mode: ORC_CLASSIFY_HEAD (the method), ORC_CLASSIFY_GQA_GROUP (every head of
+ * a KV group takes the budgets that Algorithm 3 gives the group's mean
+ * entropy) or ORC_CLASSIFY_SEGMENT (orc_budget_segment per head).  The block
+ * ranking is per query head in every mode.  A uniform budget for every head
+ * (the fixed-k scheme of CritiPrefill) is ORC_CLASSIFY_HEAD with e_t = +inf.
  * ------------------------------------------------------------------------- */
-int orc_select(const float *log_scores, const float *entropy, int B, int Hq,
-               int N, int Ls, int Lb, float e_t, double alpha, double delta_t,
-               int32_t base_budget, int32_t mult, int32_t kmax,
-               uint8_t *head_is_rigid, int32_t *budget_blocks,
-               int32_t *block_idx, int32_t *block_cnt) {
+int orc_select_mode(const float *log_scores, const float *entropy, int B, int Hq,
+                    int Hkv, int mode, int N, int Ls, int Lb, float e_t, double alpha,
+                    double delta_t, int32_t base_budget, int32_t mult, int32_t kmax,
+                    uint8_t *head_is_rigid, int32_t *budget_blocks,
+                    int32_t *block_idx, int32_t *block_cnt) {
   if (!log_scores || !entropy || !head_is_rigid || !budget_blocks || !block_idx ||
       !block_cnt)
     return ORC_ERR_ARG;
   if (B < 0 || Hq <= 0 || N < 0 || Ls <= 0 || Lb <= 0 || Ls % Lb || base_budget < 0 ||
-      mult < 1)
+      mult < 1 || Hkv <= 0 || Hq % Hkv || mode < ORC_CLASSIFY_HEAD ||
+      mode > ORC_CLASSIFY_SEGMENT)
     return ORC_ERR_ARG;
+  const int G = Hq / Hkv;
   const int64_t CS = ceil_div(N, Ls), CB = ceil_div(N, Lb), r = Ls / Lb;
   if ((int64_t)kmax < (int64_t)mult * base_budget / Lb + r) return ORC_ERR_ARG;
   int err = ORC_OK;
 #pragma omp parallel
   {
     double *Bv = (double *)malloc(sizeof(double) * (size_t)(CS > 0 ? CS : 1));
+    float *eg = (float *)malloc(sizeof(float) * (size_t)(CS > 0 ? CS : 1));
     orc_cand *cand = (orc_cand *)malloc(sizeof(orc_cand) * (size_t)(CB > 0 ? CB : 1));
     uint8_t *chosen = (uint8_t *)malloc((size_t)(CB > 0 ? CB : 1));
-    if (!Bv || !cand || !chosen) {
+    if (!Bv || !eg || !cand || !chosen) {
 #pragma omp atomic write
       err = ORC_ERR_MEM;
     }
 #pragma omp for schedule(dynamic, 1)
     for (int64_t bh = 0; bh < (int64_t)B * Hq; ++bh) {
-      if (!Bv || !cand || !chosen) continue;
+      if (!Bv || !eg || !cand || !chosen) continue;
       const float *e = entropy + bh * CS;
-      int rigid = orc_budget(e, CS, e_t, alpha, delta_t, base_budget, mult, Bv);
+      int rigid;
+      if (mode == ORC_CLASSIFY_GQA_GROUP) {
+        const int64_t first = bh - (bh % Hq) % G;   /* the group's first head */
+        orc_group_entropy(entropy + first * CS, CS, G, eg);
+        rigid = orc_budget(eg, CS, e_t, alpha, delta_t, base_budget, mult, Bv);
+      } else if (mode == ORC_CLASSIFY_SEGMENT) {
+        rigid = orc_budget_segment(e, CS, e_t, alpha, delta_t, base_budget, mult, Bv);
+      } else {
+        rigid = orc_budget(e, CS, e_t, alpha, delta_t, base_budget, mult, Bv);
+      }
       head_is_rigid[bh] = (uint8_t)rigid;
       for (int64_t s = 0; s < CS; ++s) {
         const int64_t npast = s * r;
@@ -357,10 +427,22 @@ int orc_select(const float *log_scores, const float *entropy, int B, int Hq,
       }
     }
     free(Bv);
+    free(eg);
     free(cand);
     free(chosen);
   }
   return err;
+}
+
+/* The method's selection: classification per query head (Algorithm 3). */
+int orc_select(const float *log_scores, const float *entropy, int B, int Hq,
+               int N, int Ls, int Lb, float e_t, double alpha, double delta_t,
+               int32_t base_budget, int32_t mult, int32_t kmax,
+               uint8_t *head_is_rigid, int32_t *budget_blocks,
+               int32_t *block_idx, int32_t *block_cnt) {
+  return orc_select_mode(log_scores, entropy, B, Hq, Hq, ORC_CLASSIFY_HEAD, N, Ls, Lb,
+                         e_t, alpha, delta_t, base_budget, mult, kmax, head_is_rigid,
+                         budget_blocks, block_idx, block_cnt);
 }
 
 /* ---------------------------------------------------------------------------

@@ -448,3 +448,86 @@ def test_attention_special_cases(orc):
     out0 = orc.attention(w.q, w.k, w.v, np.array([[0, h, 0] for h in range(4)], np.int32))
     for h in range(4):                            # query 0 sees only key 0
         np.testing.assert_array_equal(out0[h], from_bf16_bits(w.v[0, 0, 0]).astype(np.float64))
+
+
+# --------------------------------------------------------------------------
+# Classification variants (uniform budget, GQA-group mean, per-segment rule)
+# --------------------------------------------------------------------------
+
+def _select_k(orc, e, mode, n_kv=None, e_t=1e-5, Ls=4096, Lb=64):
+    """k_s and rigid flags of orc.select for entropies e [Hq, C_S] (random
+    scores; only the budgets are compared).  Ls = 4096 keeps n_past above
+    every budget here."""
+    e = np.asarray(e, np.float32)
+    Hq, CS = e.shape
+    N = CS * Ls
+    rng = np.random.default_rng(0)
+    ls = rng.standard_normal((1, Hq, CS, N // Lb)).astype(np.float32)
+    r = orc.select(ls, e[None], N, Ls, Lb, e_t=e_t, base_budget=2048, mult=3, mode=mode,
+                   n_kv_heads=n_kv)
+    return r["budget"][0], r["rigid"][0]
+
+
+def test_segment_rule_worked_sequence(orc):
+    """B_h = 2048, alpha B_h = 1024, Delta_t = 0.4, cap 6144; worked by hand.
+    e = [2, 1, 1e-6, 1e-6, 3, 3]:
+      per segment: s1 |1-2|/2 = 0.5 -> +102.4 = 2150.4; s2, s3 below e_t -> 2048;
+                   s4 ratio ~3e6 -> cap 6144; s5 ratio 0 -> -409.6 = 5734.4
+      per head (dynamic): s2 |1e-6-1|/1 = 0.999999 -> +614.398976 = 2764.798976;
+                   s3 -409.6 = 2355.198976; s4 cap 6144; s5 5734.4
+    k = floor(B / 64), k_0 = 0 (no past block)."""
+    e = np.asarray([2.0, 1.0, 1e-6, 1e-6, 3.0, 3.0], np.float32)
+    rg, B = orc.budget_segment(e)
+    assert not rg
+    np.testing.assert_allclose(B, [2048, 2150.4, 2048, 2048, 6144, 5734.4], rtol=1e-12)
+    rg, B = orc.budget(e)
+    np.testing.assert_allclose(B, [2048, 2150.4, 2764.798976, 2355.198976, 6144, 5734.4],
+                               rtol=1e-12)
+    k, rigid = _select_k(orc, e[None], orc.CLASSIFY_SEGMENT)
+    assert k.tolist() == [[0, 33, 32, 32, 96, 89]] and rigid.tolist() == [0]
+    k, rigid = _select_k(orc, e[None], orc.CLASSIFY_HEAD)
+    assert k.tolist() == [[0, 33, 43, 36, 96, 89]] and rigid.tolist() == [0]
+
+
+def test_segment_rule_reduces_to_head_rule(orc):
+    """All segments rigid, or none: the per-segment rule equals Algorithm 3."""
+    rng = np.random.default_rng(7)
+    for e in (rng.uniform(1e-9, 9e-6, 40), rng.uniform(1e-3, 5.0, 40)):
+        e = e.astype(np.float32)
+        a, Ba = orc.budget(e)
+        b, Bb = orc.budget_segment(e)
+        assert a == b
+        assert np.array_equal(Ba, Bb)
+
+
+def test_group_mean_entropy(orc):
+    e = np.asarray([[1.0, 2.0, 0.5], [3.0, 2.0, 0.25]], np.float32)
+    assert orc.group_entropy(e).tolist() == [2.0, 2.0, 0.375]
+    x = np.random.default_rng(3).uniform(0, 4, 50).astype(np.float32)
+    assert np.array_equal(orc.group_entropy(np.stack([x] * 7)), x)   # identical heads
+
+
+def test_group_mode_worked_example(orc):
+    """Two KV groups of two heads (e_t = 1e-5).  Group 0: both heads
+    [2, 1, 1e-6] -> the mean is the same row: B = 2048, 2150.4, 2764.798976,
+    k = 0, 33, 43.  Group 1: [1e-6]*3 and [1e-6, 1e-6, 3e-5] -> means
+    [1e-6, 1e-6, 1.55e-5], dynamic (the last mean reaches e_t): s1 ratio 0 ->
+    -409.6 -> clamp 2048; s2 |1.55e-5 - 1e-6| / 1e-6 = 14.5 -> cap 6144, so
+    k = 0, 32, 96 for both heads.  Per head, head 2 would be rigid (k = 32)."""
+    e = np.asarray([[2, 1, 1e-6], [2, 1, 1e-6], [1e-6, 1e-6, 1e-6], [1e-6, 1e-6, 3e-5]],
+                   np.float32)
+    k, rigid = _select_k(orc, e, orc.CLASSIFY_GQA_GROUP, n_kv=2)
+    assert k.tolist() == [[0, 33, 43], [0, 33, 43], [0, 32, 96], [0, 32, 96]]
+    assert rigid.tolist() == [0, 0, 0, 0]
+    k, rigid = _select_k(orc, e, orc.CLASSIFY_HEAD)
+    assert k.tolist() == [[0, 33, 43], [0, 33, 43], [0, 32, 32], [0, 32, 96]]
+    assert rigid.tolist() == [0, 0, 1, 0]
+
+
+def test_uniform_budget_is_infinite_threshold(orc):
+    """e_t = +inf classifies every head rigid: k_s = min(B_h / L_B, n_past)
+    for every head whatever its entropies (a fixed k shared by all heads)."""
+    e = np.random.default_rng(9).uniform(0, 8, (4, 6)).astype(np.float32)
+    k, rigid = _select_k(orc, e, orc.CLASSIFY_HEAD, e_t=np.inf, Ls=128)
+    assert rigid.tolist() == [1, 1, 1, 1]
+    assert k.tolist() == [[min(32, 2 * s) for s in range(6)]] * 4
