@@ -73,6 +73,19 @@ typedef struct {
   int32_t max_budget_mult;
 } ei_budget_params;
 
+/* Classification of ei_select_blocks_mode.  The block ranking is per query
+ * head in every mode; a uniform budget for all heads (the fixed k of
+ * CritiPrefill, Section 2) is EI_CLASSIFY_HEAD with entropy_threshold = +inf. */
+typedef enum {
+  EI_CLASSIFY_HEAD = 0,      /* Algorithm 3 per query head: the method */
+  EI_CLASSIFY_GQA_GROUP = 1, /* Algorithm 3 on the mean entropy of each GQA group
+                                (the per-group aggregation of Section 3); every
+                                head of the group takes the group's budgets */
+  EI_CLASSIFY_SEGMENT = 2    /* rigid rule per segment: a segment with
+                                e_s < e_t takes B_h, every other segment
+                                s >= 1 follows Algorithm 3's update from B_{s-1} */
+} ei_classify_mode;
+
 /* Version of this interface (incremented on any change of a signature). */
 int32_t ei_abi_version(void);
 
@@ -148,6 +161,24 @@ ei_status ei_select_blocks(const float* log_scores, const float* entropy, ei_dim
                            ei_tiling tiling, ei_budget_params params, int32_t kmax,
                            uint8_t* head_is_rigid, int32_t* budget_blocks,
                            int32_t* block_idx, int32_t* block_cnt, void* stream);
+
+/*
+ * ei_select_blocks_mode -- ei_select_blocks with the classification variant
+ * `mode` (an ei_classify_mode; EI_CLASSIFY_HEAD is ei_select_blocks).
+ * EI_CLASSIFY_GQA_GROUP averages the entropies of the n_q_heads / n_kv_heads
+ * query heads of each group per segment (binary64 sum in head order, divided
+ * by the group size, rounded to binary32) and runs the head rule on the mean;
+ * head_is_rigid then holds the group's flag for each of its heads.
+ * EI_CLASSIFY_SEGMENT sets B_s = B_h for every segment with e_s < e_t and
+ * otherwise applies the clamped update from B_{s-1}; head_is_rigid is set iff
+ * every segment is below e_t (then all budgets equal ei_select_blocks').
+ *
+ * Errors: as ei_select_blocks, plus EI_ERR_SHAPE for an unknown mode.
+ */
+ei_status ei_select_blocks_mode(const float* log_scores, const float* entropy, ei_dims dims,
+                                ei_tiling tiling, ei_budget_params params, int32_t mode,
+                                int32_t kmax, uint8_t* head_is_rigid, int32_t* budget_blocks,
+                                int32_t* block_idx, int32_t* block_cnt, void* stream);
 
 /*
  * ei_sparse_prefill_attn -- block-sparse causal GQA attention (Section 4.2,

@@ -73,6 +73,9 @@ def lib() -> ctypes.CDLL:
         L.ei_select_blocks.restype = ctypes.c_int
         L.ei_select_blocks.argtypes = [_VP, _VP, Dims, Tiling, BudgetParams, ctypes.c_int32, _VP,
                                        _VP, _VP, _VP, _VP]
+        L.ei_select_blocks_mode.restype = ctypes.c_int
+        L.ei_select_blocks_mode.argtypes = [_VP, _VP, Dims, Tiling, BudgetParams, ctypes.c_int32,
+                                            ctypes.c_int32, _VP, _VP, _VP, _VP, _VP]
         L.ei_sparse_prefill_attn.restype = ctypes.c_int
         L.ei_sparse_prefill_attn.argtypes = [_VP, _VP, _VP, Dims, Tiling, ctypes.c_float, _VP,
                                              _VP, ctypes.c_int32, _VP, _VP]
@@ -164,12 +167,17 @@ def entropy_probe(q, k, seg_len: int, block_len: int, probe_scale: float = 1.0,
     return log_scores, entropy
 
 
+CLASSIFY_HEAD, CLASSIFY_GQA_GROUP, CLASSIFY_SEGMENT = 0, 1, 2   # ei_classify_mode
+
+
 def select_blocks(log_scores, entropy, seq_len: int, seg_len: int, block_len: int,
                   e_t: float = 1e-5, alpha: float = 0.5, delta_t: float = 0.4,
                   base_budget: int = 2048, mult: int = 3, kmax_: int | None = None,
-                  head_dim: int = 128, n_kv_heads: int | None = None, out: dict | None = None):
-    """ei_select_blocks: returns dict(rigid u8 [B,Hq], budget i32 [B,Hq,C_S],
-    idx i32 [B,Hq,C_S,kmax], cnt i32 [B,Hq,C_S])."""
+                  head_dim: int = 128, n_kv_heads: int | None = None, out: dict | None = None,
+                  mode: int = CLASSIFY_HEAD):
+    """ei_select_blocks_mode (mode CLASSIFY_HEAD is ei_select_blocks): returns
+    dict(rigid u8 [B,Hq], budget i32 [B,Hq,C_S], idx i32 [B,Hq,C_S,kmax],
+    cnt i32 [B,Hq,C_S])."""
     _req(log_scores, "log_scores", torch.float32, 4)
     _req(entropy, "entropy", torch.float32, 3)
     B, Hq, CS, CB = log_scores.shape
@@ -188,10 +196,11 @@ def select_blocks(log_scores, entropy, seq_len: int, seg_len: int, block_len: in
     if out["idx"].shape[-1] != km:
         raise ValueError("idx last dimension must equal kmax")
     d = Dims(B, Hq, Hq if n_kv_heads is None else n_kv_heads, seq_len, head_dim)
-    _check("ei_select_blocks",
-           lib().ei_select_blocks(_ptr(log_scores), _ptr(entropy), d, Tiling(seg_len, block_len),
-                                  p, km, _ptr(out["rigid"]), _ptr(out["budget"]),
-                                  _ptr(out["idx"]), _ptr(out["cnt"]), _stream(log_scores)))
+    _check("ei_select_blocks_mode",
+           lib().ei_select_blocks_mode(_ptr(log_scores), _ptr(entropy), d,
+                                       Tiling(seg_len, block_len), p, int(mode), km,
+                                       _ptr(out["rigid"]), _ptr(out["budget"]), _ptr(out["idx"]),
+                                       _ptr(out["cnt"]), _stream(log_scores)))
     return out
 
 

@@ -8,7 +8,7 @@
 
 namespace {
 
-constexpr int32_t kAbiVersion = 1;
+constexpr int32_t kAbiVersion = 2;
 
 struct Sizes {
   int64_t B, Hq, Hkv, N, D, CS, CB, r;
@@ -118,6 +118,15 @@ ei_status ei_select_blocks(const float* log_scores, const float* entropy, ei_dim
                            ei_tiling tiling, ei_budget_params params, int32_t kmax,
                            uint8_t* head_is_rigid, int32_t* budget_blocks, int32_t* block_idx,
                            int32_t* block_cnt, void* stream) {
+  return ei_select_blocks_mode(log_scores, entropy, dims, tiling, params, EI_CLASSIFY_HEAD,
+                               kmax, head_is_rigid, budget_blocks, block_idx, block_cnt, stream);
+}
+
+ei_status ei_select_blocks_mode(const float* log_scores, const float* entropy, ei_dims dims,
+                                ei_tiling tiling, ei_budget_params params, int32_t mode,
+                                int32_t kmax, uint8_t* head_is_rigid, int32_t* budget_blocks,
+                                int32_t* block_idx, int32_t* block_cnt, void* stream) {
+  if (mode < EI_CLASSIFY_HEAD || mode > EI_CLASSIFY_SEGMENT) return EI_ERR_SHAPE;
   ei_status st = check_dims(dims);
   if (st == EI_ERR_SHAPE) return st;   // head_dim is not read by the selection
   if ((st = check_tiling(tiling)) != EI_OK) return st;
@@ -130,7 +139,7 @@ ei_status ei_select_blocks(const float* log_scores, const float* entropy, ei_dim
   const ei::SelectShape ss{(int)z.B, (int)z.Hq, (int)z.N, tiling.seg_len, tiling.block_len,
                            (int)z.CS, (int)z.CB, (int)z.r, kmax, params.entropy_threshold,
                            params.alpha, params.delta_t, params.base_budget_tokens,
-                           params.max_budget_mult};
+                           params.max_budget_mult, (int)mode, (int)(z.Hq / z.Hkv)};
   if (!ei::select_supported(ss)) return EI_ERR_UNSUPPORTED;
   return from_hip(ei::launch_select(log_scores, entropy, ss, head_is_rigid, budget_blocks,
                                     block_idx, block_cnt, (hipStream_t)stream));

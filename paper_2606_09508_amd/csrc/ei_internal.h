@@ -90,6 +90,8 @@ struct SelectShape {
   float e_t;
   double alpha, delta_t;
   int Bh, mult;
+  int mode;   // ei_classify_mode
+  int G;      // query heads per KV head
 };
 
 bool select_supported(const SelectShape& s);

@@ -5,6 +5,10 @@
 //                 segment entropies, the ratios |e_s - e_{s-1}| / e_{s-1} in
 //                 parallel, the clamped budget recurrence (inherently
 //                 sequential, one lane) and k_s = min(floor(B_s / L_B), s r).
+//                 Variants: the entropies may be the GQA group's means
+//                 (binary64 sum in head order / G, rounded to binary32), and
+//                 the rigid rule may apply per segment (B_s = B_h wherever
+//                 e_s < e_t).
 //                 binary64 with FP contraction off, in the order the budget
 //                 recurrence is written, so the result is bit-identical to any
 //                 other IEEE evaluation in that order.
@@ -17,6 +21,7 @@
 //                 resolved there with one ballot per bit.  Ties at T keep the
 //                 highest block indices; the chosen blocks plus the segment's
 //                 own blocks are written ascending.
+#include "../../include/entropyinfer.h"
 #include "ei_internal.h"
 
 #include <math.h>
@@ -30,19 +35,28 @@ constexpr int kThreads = 256;
 constexpr int kChunk = 1024;
 
 __global__ __launch_bounds__(kThreads) void budget_kernel(
-    const float* __restrict__ entropy, int CS, int r, int Lb, float e_t, double alpha,
-    double delta_t, int Bh, int mult, uint8_t* __restrict__ rigid_out,
+    const float* __restrict__ entropy, int Hq, int CS, int r, int Lb, float e_t, double alpha,
+    double delta_t, int Bh, int mult, int mode, int G, uint8_t* __restrict__ rigid_out,
     int32_t* __restrict__ k_out) {
   __shared__ double delta[kChunk];
   __shared__ double Bs[kChunk];
+  __shared__ unsigned char seg_rigid[kChunk];
   const int64_t bh = blockIdx.x;
-  const float* e = entropy + bh * CS;
   int32_t* ko = k_out + bh * CS;
   const int tid = threadIdx.x;
+  // the entropy row this head's budgets follow
+  const bool group = mode == EI_CLASSIFY_GQA_GROUP;
+  const float* e = entropy + (group ? bh - (bh % Hq) % G : bh) * CS;
+  auto E = [&](int s) -> float {
+    if (!group) return e[s];
+    double sum = 0.0;
+    for (int h = 0; h < G; ++h) sum += (double)e[(int64_t)h * CS + s];
+    return (float)(sum / (double)G);
+  };
 
   int below = 1;
   for (int s = tid; s < CS; s += kThreads)
-    if (!(e[s] < e_t)) below = 0;
+    if (!(E(s) < e_t)) below = 0;
   below = __syncthreads_and(below);
   const double B0 = (double)Bh;
   const double cap = (double)mult * B0;
@@ -59,8 +73,10 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(
     const int n = min(kChunk, CS - c0);
     for (int i = tid; i < n; i += kThreads) {
       const int s = c0 + i;
-      if (s == 0) { delta[i] = 0.0; continue; }
-      const double ep = (double)e[s - 1], ec = (double)e[s];
+      if (s == 0) { delta[i] = 0.0; seg_rigid[i] = 0; continue; }
+      const float es = E(s);
+      seg_rigid[i] = (mode == EI_CLASSIFY_SEGMENT && es < e_t) ? 1 : 0;
+      const double ep = (double)E(s - 1), ec = (double)es;
       const double num = fabs(ec - ep);
       const double ratio = (num == 0.0 && ep == 0.0) ? 0.0 : num / ep;
       const double t = ratio - delta_t;
@@ -70,7 +86,7 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(
     if (tid == 0) {
       for (int i = 0; i < n; ++i) {
         double Bn;
-        if (c0 + i == 0) {
+        if (c0 + i == 0 || seg_rigid[i]) {
           Bn = B0;
         } else {
           Bn = Bprev + delta[i];
@@ -304,8 +320,8 @@ hipError_t launch_select(const float* log_scores, const float* entropy, const Se
                          uint8_t* rigid, int32_t* budget_blocks, int32_t* block_idx,
                          int32_t* block_cnt, hipStream_t stream) {
   hipLaunchKernelGGL(budget_kernel, dim3((unsigned)(s.B * s.Hq)), dim3(kThreads), 0, stream,
-                     entropy, s.CS, s.r, s.Lb, s.e_t, s.alpha, s.delta_t, s.Bh, s.mult, rigid,
-                     budget_blocks);
+                     entropy, s.Hq, s.CS, s.r, s.Lb, s.e_t, s.alpha, s.delta_t, s.Bh, s.mult,
+                     s.mode, s.G, rigid, budget_blocks);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int npast_max = (s.CS - 1) * s.r;

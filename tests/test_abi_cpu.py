@@ -35,7 +35,7 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_helpers(L):
-    assert L.ei_abi_version() == 1
+    assert L.ei_abi_version() == 2
     assert eb.kmax(128, 64, 2048, 3) == 98
     assert eb.kmax(2048, 64, 2048, 3) == 96 + 32
     assert eb.kmax(256, 128, 256, 3) == 6 + 2
@@ -101,6 +101,10 @@ def test_select_rejects_bad_params(L):
                               *args) == -2
     assert L.ei_select_blocks(FAKE, None, d, t, p, km, *args) == -1
     assert L.ei_select_blocks(FAKE, FAKE, d, t, p, km, FAKE, FAKE, None, FAKE, None) == -1
+    for mode in (-1, 3, 100):
+        assert L.ei_select_blocks_mode(FAKE, FAKE, d, t, p, mode, km, *args) == -2
+    assert L.ei_select_blocks_mode(FAKE, FAKE, d, t, p, 1, km - 1, *args) == -2
+    assert L.ei_select_blocks_mode(FAKE, None, d, t, p, 2, km, *args) == -1
 
 
 def test_attention_rejects_bad_arguments(L):

@@ -250,6 +250,47 @@ def test_select_crafted_scores():
             np.testing.assert_array_equal(g[name], ref[name], err_msg=f"{name} B_h={bh}")
 
 
+@pytest.mark.parametrize("mode", [eb.CLASSIFY_HEAD, eb.CLASSIFY_GQA_GROUP, eb.CLASSIFY_SEGMENT])
+@pytest.mark.parametrize("e_t", [1e-5, math.inf])
+def test_select_modes_match_oracle(mode, e_t):
+    """Every classification variant, bit-exact against the oracle on the GPU's
+    own probe outputs (e_t = +inf: the uniform budget)."""
+    w = synth.make("c2", 1, N=16384)
+    q, k = to_dev(w.q), to_dev(w.k)
+    ls, en = eb.entropy_probe(q, k, w.Ls, w.Lb, w.probe_scale)
+    sel = eb.select_blocks(ls, en, w.N, w.Ls, w.Lb, e_t, w.alpha, w.delta_t, w.base_budget,
+                           w.mult, n_kv_heads=w.Hkv, mode=mode)
+    torch.cuda.synchronize()
+    g = {kk: t.cpu().numpy() for kk, t in sel.items()}
+    ref = oracle.select(ls.cpu().numpy(), en.cpu().numpy(), w.N, w.Ls, w.Lb, e_t, w.alpha,
+                        w.delta_t, w.base_budget, w.mult, mode=mode, n_kv_heads=w.Hkv)
+    for name in ("rigid", "budget", "cnt", "idx"):
+        np.testing.assert_array_equal(g[name], ref[name], err_msg=f"{name} mode={mode}")
+    if e_t == math.inf:
+        assert g["rigid"].all()
+
+
+def test_select_mode_worked_budgets_on_gpu():
+    """The hand-worked variant budgets (see the oracle pins) on the GPU."""
+    Ls, Lb = 4096, 64
+    e = np.asarray([[2, 1, 1e-6, 1e-6, 3, 3]] * 2 + [[2, 1, 1e-6, 1e-6, 1e-6, 1e-6],
+                                                    [2, 1, 1e-6, 1e-6, 1e-6, 3e-5]], np.float32)
+    Hq, CS = e.shape
+    N = CS * Ls
+    ls = torch.zeros((1, Hq, CS, N // Lb), dtype=torch.float32, device="cuda")
+    en = torch.from_numpy(e[None]).cuda()
+    got = {}
+    for mode in (eb.CLASSIFY_HEAD, eb.CLASSIFY_GQA_GROUP, eb.CLASSIFY_SEGMENT):
+        sel = eb.select_blocks(ls, en, N, Ls, Lb, 1e-5, 0.5, 0.4, 2048, 3, n_kv_heads=2,
+                               mode=mode)
+        got[mode] = sel["budget"][0].cpu().numpy().tolist()
+    assert got[eb.CLASSIFY_SEGMENT][0] == [0, 33, 32, 32, 96, 89]
+    assert got[eb.CLASSIFY_HEAD][0] == [0, 33, 43, 36, 96, 89]
+    assert got[eb.CLASSIFY_GQA_GROUP][0] == got[eb.CLASSIFY_HEAD][0]        # identical heads
+    # group 1: heads 2 and 3 share the budgets of their mean entropy
+    assert got[eb.CLASSIFY_GQA_GROUP][2] == got[eb.CLASSIFY_GQA_GROUP][3]
+
+
 def _sample_rows(w, n_seg=48, seed=0):
     rng = np.random.default_rng(seed)
     segs = np.unique(np.concatenate([[0, 1, w.CS - 1], rng.integers(0, w.CS, n_seg)]))
