@@ -111,6 +111,9 @@ def main():
     ap.add_argument("--dense-reps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
+    ap.add_argument("--sweep", action="store_true",
+                    help="instead of the benchmark line, time the classification variants and "
+                         "the L_S / B_h sweeps on the same layer and print a markdown table")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run one device-to-device copy of this size, so that a "
                          "rocprofv3 --pmc run can scale FETCH_SIZE / WRITE_SIZE by it")
@@ -139,6 +142,9 @@ def main():
         return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
 
     q, k, v = to_dev(w.q), to_dev(w.k), to_dev(w.v)
+    if args.sweep:
+        sweep(args, w, q, k, v)
+        return
     if args.calibrate_copy_mib > 0:
         n = args.calibrate_copy_mib << 20
         src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
@@ -275,6 +281,96 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def time_path(w, q, k, v, Ls, Lb, base_budget, e_t, mode, steps, warmup):
+    """Mean per-stage milliseconds of probe -> select -> sparse attention for
+    one variant, plus its selection (for work counts)."""
+    import torch
+    from paper_2606_09508_amd import binding as eb
+
+    CS, CB = -(-w.N // Ls), -(-w.N // Lb)
+    km = eb.kmax(Ls, Lb, base_budget, w.mult)
+    dev = q.device
+    ls = torch.empty((w.B, w.Hq, CS, CB), dtype=torch.float32, device=dev)
+    en = torch.empty((w.B, w.Hq, CS), dtype=torch.float32, device=dev)
+    ws = torch.empty((eb.probe_workspace_bytes(eb.dims_of(q, k), Ls, Lb),), dtype=torch.uint8,
+                     device=dev)
+    sel = {"rigid": torch.empty((w.B, w.Hq), dtype=torch.uint8, device=dev),
+           "budget": torch.empty((w.B, w.Hq, CS), dtype=torch.int32, device=dev),
+           "idx": torch.empty((w.B, w.Hq, CS, km), dtype=torch.int32, device=dev),
+           "cnt": torch.empty((w.B, w.Hq, CS), dtype=torch.int32, device=dev)}
+    o = torch.empty_like(q)
+
+    def one(ev=None):
+        if ev is not None:
+            ev[0].record()
+        eb.entropy_probe(q, k, Ls, Lb, w.probe_scale, ls, en, ws)
+        if ev is not None:
+            ev[1].record()
+        eb.select_blocks(ls, en, w.N, Ls, Lb, e_t, w.alpha, w.delta_t, base_budget, w.mult,
+                         n_kv_heads=w.Hkv, out=sel, mode=mode)
+        if ev is not None:
+            ev[2].record()
+        eb.sparse_prefill_attn(q, k, v, sel["idx"], sel["cnt"], Ls, Lb, w.softmax_scale, o)
+        if ev is not None:
+            ev[3].record()
+
+    for _ in range(warmup):
+        one()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    for e in evs:
+        one(e)
+    torch.cuda.synchronize()
+    st = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
+                   for e in evs]).mean(axis=0)
+    cnt = sel["cnt"].cpu().numpy()
+    idx = sel["idx"].cpu().numpy()
+    rigid = sel["rigid"].cpu().numpy()
+    return st, cnt, idx, rigid
+
+
+def sweep(args, w, q, k, v):
+    """Kernel-level cost of the classification variants and of L_S / B_h on
+    one layer (markdown table on stdout)."""
+    import torch
+    from paper_2606_09508_amd import binding as eb
+
+    steps, warmup = max(3, min(args.steps, 10)), max(1, min(args.warmup, 3))
+    od = torch.empty_like(q)
+    eb.dense_prefill_attn(q, k, v, w.softmax_scale, True, od)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    eb.dense_prefill_attn(q, k, v, w.softmax_scale, True, od)
+    e1.record()
+    torch.cuda.synchronize()
+    dense_ms = e0.elapsed_time(e1)
+    dense_pairs = w.B * w.Hq * w.N * (w.N + 1) // 2
+    names = {eb.CLASSIFY_HEAD: "per head (the method)", eb.CLASSIFY_GQA_GROUP: "GQA-group mean",
+             eb.CLASSIFY_SEGMENT: "per segment"}
+    configs = [(names[m], w.Ls, w.base_budget, w.e_t, m)
+               for m in (eb.CLASSIFY_HEAD, eb.CLASSIFY_GQA_GROUP, eb.CLASSIFY_SEGMENT)]
+    configs.append(("uniform budget (e_t = +inf)", w.Ls, w.base_budget, math.inf,
+                    eb.CLASSIFY_HEAD))
+    configs += [("per head", ls_, w.base_budget, w.e_t, eb.CLASSIFY_HEAD)
+                for ls_ in (256, 512, 1024, 2048)]
+    configs += [("per head", w.Ls, bh, w.e_t, eb.CLASSIFY_HEAD) for bh in (1024, 4096)]
+    print(f"Layer: {w.Hq} query / {w.Hkv} KV heads, N = {w.N}, D = {w.D}, L_B = {w.Lb}, "
+          f"seed {args.seed}; dense causal attention {dense_ms:.2f} ms; "
+          f"{steps} timed steps after {warmup} warm-up per row.\n")
+    print("| classification | L_S | B_h | rigid heads | computed pairs | probe ms | select ms "
+          "| sparse attn ms | total ms | sparse TFLOP/s | speedup vs dense |")
+    print("|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|")
+    for name, Ls, bh, e_t, mode in configs:
+        st, cnt, idx, rigid = time_path(w, q, k, v, Ls, w.Lb, bh, e_t, mode, steps, warmup)
+        pairs = causal_pairs(cnt, idx, w.N, Ls, w.Lb)
+        tot = float(st.sum())
+        print(f"| {name} | {Ls} | {bh} | {int(rigid.sum())}/{w.B * w.Hq} | "
+              f"{pairs / dense_pairs:.4f} | {st[0]:.3f} | {st[1]:.3f} | {st[2]:.3f} | {tot:.3f} | "
+              f"{4.0 * w.D * pairs / (st[2] * 1e-3) / 1e12:.0f} | {dense_ms / tot:.2f} |",
+              flush=True)
 
 
 def cpu_baseline(w, bufs, cnt, idx, pairs, budget_s):
