@@ -349,3 +349,40 @@ def test_c3_dense_sampled(c3):
     ref = oracle.attention(w.q, w.k, w.v, rows, w.softmax_scale, True)
     got = bf16_to_f64(od)[rows[:, 0], rows[:, 1], rows[:, 2]]
     assert np.abs(got - ref).max() <= ATTN_ABS
+
+
+def test_c4_qwen7b_64k_sampled():
+    """Qwen2.5-7B layer shape (G = 7), 65536 tokens, lognormal key norms and
+    retrieval spans: sampled probe rows and query rows, full selection."""
+    w = synth.make("c4", 0)
+    say("[c4] generated")
+    r = run_path(w)
+    hrel, lerr = check_probe(w, r, _sample_rows(w, n_seg=32, seed=2))
+    check_select(w, r)
+    amax, amean = check_attention(w, r, _sample_query_rows(w, n=48, seed=3))
+    say(f"  entropy rel {hrel:.2e} L {lerr:.2e} attn {amax:.2e}/{amean:.2e}")
+
+
+def test_c5_llama70b_128k_sampled():
+    """Llama-3-70B layer on one GPU (64 query / 8 KV heads), 131072 tokens:
+    sampled probe and attention rows; selection bit-exact at e_t = 1e-6,
+    1e-5 and 1e-4."""
+    w = synth.make("c5", 0)
+    say("[c5] generated")
+    r = run_path(w)
+    hrel, lerr = check_probe(w, r, _sample_rows(w, n_seg=24, seed=4))
+    check_select(w, r)
+    for e_t in (1e-6, 1e-4):
+        ls = torch.from_numpy(r["ls"]).cuda()
+        en = torch.from_numpy(r["en"]).cuda()
+        sel = eb.select_blocks(ls, en, w.N, w.Ls, w.Lb, e_t, w.alpha, w.delta_t, w.base_budget,
+                               w.mult, n_kv_heads=w.Hkv)
+        torch.cuda.synchronize()
+        ref = oracle.select(r["ls"], r["en"], w.N, w.Ls, w.Lb, e_t, w.alpha, w.delta_t,
+                            w.base_budget, w.mult)
+        for name in ("rigid", "budget", "cnt", "idx"):
+            np.testing.assert_array_equal(sel[name].cpu().numpy(), ref[name],
+                                          err_msg=f"{name} e_t={e_t}")
+        del ls, en, sel
+    amax, amean = check_attention(w, r, _sample_query_rows(w, n=32, seed=6))
+    say(f"  entropy rel {hrel:.2e} L {lerr:.2e} attn {amax:.2e}/{amean:.2e}")
