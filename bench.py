@@ -198,6 +198,27 @@ def main():
     probe_ms, select_ms, sparse_ms = [float(x) for x in st.mean(axis=0)]
     pct = np.percentile(st, [10, 50, 90], axis=0)
 
+    # probe and select with cold caches: a 512 MB write evicts L2 and MALL
+    # before each (both are HBM-bound; inside the step they follow attention)
+    flush = torch.empty((512 << 20,), dtype=torch.uint8, device=dev)
+    cold = {"probe": [], "select": []}
+    for rep in range(5):
+        for stage in ("probe", "select"):
+            flush.fill_(rep + 1)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            if stage == "probe":
+                eb.entropy_probe(q, k, w.Ls, w.Lb, w.probe_scale, bufs["log_scores"],
+                                 bufs["entropy"], bufs["workspace"])
+            else:
+                eb.select_blocks(bufs["log_scores"], bufs["entropy"], w.N, w.Ls, w.Lb, w.e_t,
+                                 w.alpha, w.delta_t, w.base_budget, w.mult, n_kv_heads=w.Hkv,
+                                 out=bufs["sel"])
+            e1.record()
+            torch.cuda.synchronize()
+            cold[stage].append(e0.elapsed_time(e1))
+    del flush
+
     # dense baseline on the same inputs
     od = torch.empty_like(q)
     eb.dense_prefill_attn(q, k, v, w.softmax_scale, True, od)
@@ -265,6 +286,7 @@ def main():
                       "sparse_attn": round(sparse_ms, 4)},
         "stages_ms_p10_p50_p90": {name: [round(float(x), 4) for x in pct[:, i]]
                                   for i, name in enumerate(("probe", "select", "sparse_attn"))},
+        "stages_ms_cold_cache": {k_: round(float(np.median(v_)), 4) for k_, v_ in cold.items()},
         "mfma_util": round(sparse_tflops / PEAK_BF16_TFLOPS, 4),
         "sparse_attn_tflops": round(sparse_tflops, 2),
         "sparse_attn_tile_tflops": round(sparse_tile_tflops, 2),
@@ -424,18 +446,44 @@ def cpu_baseline(w, bufs, cnt, idx, pairs, budget_s):
     if n > 1024:
         qrows = query_rows(n)
         t_att = time_attention(qrows)
-    sample_pairs = 0
-    for c0 in range(0, len(qrows), 1 << 15):
-        qb = qrows[c0:c0 + (1 << 15)]
-        seg = qb[:, 2] // w.Ls
-        blk = idx[qb[:, 0], qb[:, 1], seg].astype(np.int64)               # [n, kmax]
-        live = np.arange(blk.shape[1])[None, :] < cnt[qb[:, 0], qb[:, 1], seg][:, None]
-        k0 = blk * w.Lb
-        k1 = np.minimum(k0 + w.Lb, w.N)
-        span = np.minimum(k1, qb[:, 2:3].astype(np.int64) + 1) - k0
-        sample_pairs += int(np.where(live, np.maximum(span, 0), 0).sum())
-    att_full = t_att * pairs / max(sample_pairs, 1)
+    def pairs_of(qr):
+        n_p = 0
+        for c0 in range(0, len(qr), 1 << 15):
+            qb = qr[c0:c0 + (1 << 15)]
+            seg = qb[:, 2] // w.Ls
+            blk = idx[qb[:, 0], qb[:, 1], seg].astype(np.int64)               # [n, kmax]
+            live = np.arange(blk.shape[1])[None, :] < cnt[qb[:, 0], qb[:, 1], seg][:, None]
+            k0 = blk * w.Lb
+            k1 = np.minimum(k0 + w.Lb, w.N)
+            span = np.minimum(k1, qb[:, 2:3].astype(np.int64) + 1) - k0
+            n_p += int(np.where(live, np.maximum(span, 0), 0).sum())
+        return max(n_p, 1)
+
+    att_full = t_att * pairs / pairs_of(qrows)
     total_s = probe_full + t_sel + att_full
+
+    # dense causal attention in the oracle, on sampled query rows, scaled by
+    # the causal pair count (extrapolated)
+    qd = query_rows(256)
+    t0 = time.perf_counter()
+    oracle.attention(w.q, w.k, w.v, qd, w.softmax_scale, True)
+    t_dense = time.perf_counter() - t0
+    dense_full = t_dense * (w.B * w.Hq * w.N * (w.N + 1) / 2) / float((qd[:, 2] + 1).sum())
+
+    # one thread: smaller samples of the same kinds
+    oracle.set_threads(1)
+    try:
+        rows1 = probe_rows(4)
+        probe1 = time_probe(rows1) * (w.B * w.Hq * nvis.sum()) / nvis[rows1[:, 2]].sum()
+        t0 = time.perf_counter()
+        oracle.select(ls, en, w.N, w.Ls, w.Lb, w.e_t, w.alpha, w.delta_t, w.base_budget, w.mult)
+        sel1 = time.perf_counter() - t0
+        q1 = query_rows(1024)
+        att1 = time_attention(q1) * pairs / pairs_of(q1)
+    finally:
+        oracle.set_threads(cores)
+    single = {"value": round((probe1 + sel1 + att1) * 1e3, 1), "unit": "ms/layer", "cores": 1,
+              "sample": f"probe: {len(rows1)} rows; select: whole layer; attention: 1024 rows"}
     return {"value": round(total_s * 1e3, 1), "unit": "ms/layer", "cores": cores,
             "kind": "oracle",
             "sample": (f"probe: {len(rows)} (head, segment) rows at {len(rows) // w.Hq} segment "
@@ -443,7 +491,9 @@ def cpu_baseline(w, bufs, cnt, idx, pairs, budget_s):
                        f"scaled by visible blocks; select: whole layer, {t_sel:.2f}s; attention: "
                        f"{len(qrows)} random query rows, {t_att:.2f}s, scaled by causal pairs"),
             "stages_s": {"probe": round(probe_full, 2), "select": round(t_sel, 2),
-                         "sparse_attn": round(att_full, 2)}}
+                         "sparse_attn": round(att_full, 2)},
+            "dense_attn_s_extrapolated": round(dense_full, 1),
+            "single_core": single}
 
 
 if __name__ == "__main__":

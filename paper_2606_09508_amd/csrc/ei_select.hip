@@ -38,9 +38,8 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(
     const float* __restrict__ entropy, int Hq, int CS, int r, int Lb, float e_t, double alpha,
     double delta_t, int Bh, int mult, int mode, int G, uint8_t* __restrict__ rigid_out,
     int32_t* __restrict__ k_out) {
-  __shared__ double delta[kChunk];
+  __shared__ double delta[kChunk];   // -inf: the segment restarts at B_h
   __shared__ double Bs[kChunk];
-  __shared__ unsigned char seg_rigid[kChunk];
   const int64_t bh = blockIdx.x;
   int32_t* ko = k_out + bh * CS;
   const int tid = threadIdx.x;
@@ -73,9 +72,13 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(
     const int n = min(kChunk, CS - c0);
     for (int i = tid; i < n; i += kThreads) {
       const int s = c0 + i;
-      if (s == 0) { delta[i] = 0.0; seg_rigid[i] = 0; continue; }
       const float es = E(s);
-      seg_rigid[i] = (mode == EI_CLASSIFY_SEGMENT && es < e_t) ? 1 : 0;
+      // B_0 = B_h, and a rigid segment of the per-segment rule takes B_h:
+      // B_prev + (-inf) is clamped to exactly B_h below
+      if (s == 0 || (mode == EI_CLASSIFY_SEGMENT && es < e_t)) {
+        delta[i] = -INFINITY;
+        continue;
+      }
       const double ep = (double)E(s - 1), ec = (double)es;
       const double num = fabs(ec - ep);
       const double ratio = (num == 0.0 && ep == 0.0) ? 0.0 : num / ep;
@@ -85,14 +88,9 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(
     __syncthreads();
     if (tid == 0) {
       for (int i = 0; i < n; ++i) {
-        double Bn;
-        if (c0 + i == 0 || seg_rigid[i]) {
-          Bn = B0;
-        } else {
-          Bn = Bprev + delta[i];
-          if (!(Bn >= B0)) Bn = B0;
-          if (Bn > cap) Bn = cap;
-        }
+        double Bn = Bprev + delta[i];
+        if (!(Bn >= B0)) Bn = B0;
+        if (Bn > cap) Bn = cap;
         Bs[i] = Bn;
         Bprev = Bn;
       }
