@@ -118,6 +118,9 @@ C1_CASES = [
     dict(Ls=2048, Lb=64, N=4096, base_budget=1024),
     dict(N=2048, base_budget=64),                     # k = 1 past block
     dict(N=2048, base_budget=0),                      # own blocks only
+    dict(N=1),                                        # one token
+    dict(N=65),                                       # one full block and one row
+    dict(B=3, Hq=1, Hkv=1, N=200),                    # single head, batch of three
 ]
 
 
@@ -385,4 +388,19 @@ def test_c5_llama70b_128k_sampled():
                                           err_msg=f"{name} e_t={e_t}")
         del ls, en, sel
     amax, amean = check_attention(w, r, _sample_query_rows(w, n=32, seed=6))
+    say(f"  entropy rel {hrel:.2e} L {lerr:.2e} attn {amax:.2e}/{amean:.2e}")
+
+
+def test_maximum_block_count():
+    """The largest C_B the selector supports (8192 key blocks: N = 524288 at
+    L_B = 64), one head: probe rows up to 8192 visible blocks, the 128-slot
+    selector, sampled attention rows."""
+    w = synth.make("c1", 7, N=524288, Hq=1, Hkv=1, base_budget=2048)
+    assert w.CB == 8192
+    say("[max] generated")
+    r = run_path(w)
+    rows = np.array([[0, 0, s] for s in (0, 1, 2047, 4094, 4095)], np.int32)
+    hrel, lerr = check_probe(w, r, rows)
+    check_select(w, r)
+    amax, amean = check_attention(w, r, _sample_query_rows(w, n=16, seed=8))
     say(f"  entropy rel {hrel:.2e} L {lerr:.2e} attn {amax:.2e}/{amean:.2e}")
