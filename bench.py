@@ -5,6 +5,11 @@ resident in HBM: entropy probe -> head classification, budgets and top-k
 selection -> block-sparse causal GQA attention.  The default workload is the
 Llama-3-8B attention layer at 131072 tokens (Hq=32, Hkv=8, D=128, L_S=128,
 L_B=64, B_h=2048).  Prints one JSON line; see the keys below.
+
+``value`` / ``ms_per_step`` time the library's one-call path for the layer
+(ei_entropy_guided_prefill: the stages pipelined over KV-head groups on two
+streams); ``stages_ms`` and ``serial_ms_per_step`` time the three separate
+calls on one stream, whose sparse-attention launch gives the roofline.
 """
 from __future__ import annotations
 
@@ -198,6 +203,31 @@ def main():
     probe_ms, select_ms, sparse_ms = [float(x) for x in st.mean(axis=0)]
     pct = np.percentile(st, [10, 50, 90], axis=0)
 
+    # the product's step: ei_entropy_guided_prefill, the same three stages
+    # pipelined over KV-head groups on two streams (bitwise the same outputs)
+    pbufs = {}
+
+    def pstep():
+        eb.entropy_guided_prefill(q, k, v, w.Ls, w.Lb, w.base_budget, w.e_t, w.alpha,
+                                  w.delta_t, w.mult, w.probe_scale, w.softmax_scale, bufs=pbufs)
+
+    for _ in range(args.warmup):
+        pstep()
+    pev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for e in pev:
+        e[0].record()
+        pstep()
+        e[1].record()
+    torch.cuda.synchronize()
+    pipe_wall_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    pipe_all = np.array([e[0].elapsed_time(e[1]) for e in pev])
+    pipe_ms = float(pipe_all.mean())
+    if not torch.equal(pbufs["out"], bufs["out"]):
+        print("pipelined output differs from the separate calls", file=sys.stderr)
+        sys.exit(1)
+
     # probe and select with cold caches: a 512 MB write evicts L2 and MALL
     # before each (both are HBM-bound; inside the step they follow attention)
     flush = torch.empty((512 << 20,), dtype=torch.uint8, device=dev)
@@ -264,13 +294,17 @@ def main():
 
     out = {
         "metric": METRIC,
-        "value": round(total_ms, 4),
+        "value": round(pipe_ms, 4),
         "unit": "ms/layer",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(total_ms, 4),
-        "wall_ms_per_step": round(wall_ms, 4),
+        "ms_per_step": round(pipe_ms, 4),
+        "wall_ms_per_step": round(pipe_wall_ms, 4),
+        "ms_per_step_p10_p50_p90": [round(float(x), 4)
+                                    for x in np.percentile(pipe_all, [10, 50, 90])],
+        "serial_ms_per_step": round(total_ms, 4),
+        "serial_wall_ms_per_step": round(wall_ms, 4),
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
@@ -293,7 +327,7 @@ def main():
         "mfma_busy_counter": read_counter_file(SQ_FILE, "mfma_busy_fraction"),
         "dense_ms": round(dense_ms, 3),
         "dense_tflops": round(dense_tflops, 2),
-        "speedup_vs_dense": round(dense_ms / total_ms, 3),
+        "speedup_vs_dense": round(dense_ms / pipe_ms, 3),
         "computed_pair_fraction": round(pairs / dense_pairs, 4),
         "probe_hbm_gbs": round(probe_bytes / (probe_ms * 1e-3) / 1e9, 1),
         "select_hbm_gbs": round(select_bytes / (select_ms * 1e-3) / 1e9, 1),

@@ -216,6 +216,46 @@ ei_status ei_dense_prefill_attn(const uint16_t* q, const uint16_t* k, const uint
                                 ei_dims dims, float softmax_scale, int32_t causal,
                                 uint16_t* o, void* stream);
 
+/* Workspace bytes ei_entropy_guided_prefill needs (the probe workspace of
+ * one KV-head group, reused group after group); 0 on invalid sizes. */
+size_t ei_prefill_workspace_bytes(ei_dims dims, ei_tiling tiling);
+
+/*
+ * ei_entropy_guided_prefill -- the whole prefill path of one layer (Section
+ * 4.2): ei_entropy_probe, ei_select_blocks_mode and ei_sparse_prefill_attn for
+ * every head.  From N = 16384 tokens on the stages are pipelined over
+ * (batch, KV-head group): the probe of group g+1 runs on `stream` while the
+ * selection and sparse attention of group g run on `stream_aux`.  Below that
+ * the per-group launches cost more than the overlap gains, and the call runs
+ * the probes group by group, then one selection and one attention launch over
+ * all heads, on `stream` alone.  Every kernel sees exactly the data it would
+ * see in the three separate calls, so all outputs are bitwise identical to
+ * them either way.
+ *
+ *   q, k, v            as ei_sparse_prefill_attn
+ *   probe_scale        as ei_entropy_probe; softmax_scale as the attention
+ *   params, mode, kmax as ei_select_blocks_mode
+ *   log_scores, entropy, head_is_rigid, budget_blocks, block_idx, block_cnt,
+ *   o                  outputs of the three calls (same layouts)
+ *   workspace          at least ei_prefill_workspace_bytes()
+ *   stream, stream_aux hipStream_t, distinct (NULL = the default stream is
+ *                      allowed for `stream` only).  On return `stream` is
+ *                      ordered after all the work: synchronising `stream`
+ *                      makes every output valid.  Both streams must be of
+ *                      default priority.
+ *
+ * Errors: those of the three calls, plus EI_ERR_SHAPE if stream_aux is NULL
+ * or equal to stream, and EI_ERR_LAUNCH if an event cannot be created.
+ */
+ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                                    ei_dims dims, ei_tiling tiling, double probe_scale,
+                                    ei_budget_params params, int32_t mode, int32_t kmax,
+                                    float softmax_scale, float* log_scores, float* entropy,
+                                    uint8_t* head_is_rigid, int32_t* budget_blocks,
+                                    int32_t* block_idx, int32_t* block_cnt, uint16_t* o,
+                                    void* workspace, size_t workspace_bytes, void* stream,
+                                    void* stream_aux);
+
 #ifdef __cplusplus
 }
 #endif

@@ -79,6 +79,13 @@ def lib() -> ctypes.CDLL:
         L.ei_sparse_prefill_attn.restype = ctypes.c_int
         L.ei_sparse_prefill_attn.argtypes = [_VP, _VP, _VP, Dims, Tiling, ctypes.c_float, _VP,
                                              _VP, ctypes.c_int32, _VP, _VP]
+        L.ei_prefill_workspace_bytes.restype = ctypes.c_size_t
+        L.ei_prefill_workspace_bytes.argtypes = [Dims, Tiling]
+        L.ei_entropy_guided_prefill.restype = ctypes.c_int
+        L.ei_entropy_guided_prefill.argtypes = [_VP, _VP, _VP, Dims, Tiling, ctypes.c_double,
+                                                BudgetParams, ctypes.c_int32, ctypes.c_int32,
+                                                ctypes.c_float, _VP, _VP, _VP, _VP, _VP, _VP,
+                                                _VP, _VP, ctypes.c_size_t, _VP, _VP]
         L.ei_dense_prefill_attn.restype = ctypes.c_int
         L.ei_dense_prefill_attn.argtypes = [_VP, _VP, _VP, Dims, ctypes.c_float, ctypes.c_int32,
                                             _VP, _VP]
@@ -247,20 +254,63 @@ def dense_prefill_attn(q, k, v, softmax_scale: float | None = None, causal: bool
     return out
 
 
+_AUX_STREAMS: dict = {}
+
+
+def _aux_stream(device) -> torch.cuda.Stream:
+    """A second stream per device (default priority) for the pipelined path."""
+    idx = torch.device(device).index or 0
+    if idx not in _AUX_STREAMS:
+        _AUX_STREAMS[idx] = torch.cuda.Stream(device=idx)
+    return _AUX_STREAMS[idx]
+
+
+def prefill_workspace_bytes(dims: Dims, seg_len: int, block_len: int) -> int:
+    return int(lib().ei_prefill_workspace_bytes(dims, Tiling(seg_len, block_len)))
+
+
 def entropy_guided_prefill(q, k, v, seg_len: int = 128, block_len: int = 64,
                            base_budget: int = 2048, e_t: float = 1e-5, alpha: float = 0.5,
                            delta_t: float = 0.4, mult: int = 3, probe_scale: float = 1.0,
-                           softmax_scale: float | None = None, bufs: dict | None = None):
-    """The whole hot path on one layer: probe -> select -> sparse attention.
-
-    ``bufs`` (optional) caches the intermediate device buffers between calls.
-    Returns (output, selection dict, log_scores, entropy).
-    """
+                           softmax_scale: float | None = None, bufs: dict | None = None,
+                           mode: int = CLASSIFY_HEAD):
+    """ei_entropy_guided_prefill: the whole path on one layer (probe -> select
+    -> sparse attention), pipelined over KV-head groups on the current stream
+    and a second stream.  ``bufs`` (optional) caches the output and scratch
+    buffers between calls.  Returns (output, selection dict, log_scores,
+    entropy)."""
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _req(t, n, torch.bfloat16, 4)
+    d = dims_of(q, k)
+    B, Hq, N, D = q.shape
+    CS, CB = num_segments(N, seg_len), num_blocks(N, block_len)
+    km = kmax(seg_len, block_len, base_budget, mult)
+    dev = q.device
     bufs = {} if bufs is None else bufs
-    ls, en = entropy_probe(q, k, seg_len, block_len, probe_scale, bufs.get("log_scores"),
-                           bufs.get("entropy"), bufs.get("workspace"))
-    sel = select_blocks(ls, en, q.shape[2], seg_len, block_len, e_t, alpha, delta_t, base_budget,
-                        mult, n_kv_heads=k.shape[1], out=bufs.get("sel"))
-    o = sparse_prefill_attn(q, k, v, sel["idx"], sel["cnt"], seg_len, block_len, softmax_scale,
-                            bufs.get("out"))
-    return o, sel, ls, en
+    shapes = {"log_scores": ((B, Hq, CS, CB), torch.float32), "entropy": ((B, Hq, CS), torch.float32),
+              "rigid": ((B, Hq), torch.uint8), "budget": ((B, Hq, CS), torch.int32),
+              "idx": ((B, Hq, CS, km), torch.int32), "cnt": ((B, Hq, CS), torch.int32),
+              "out": (tuple(q.shape), torch.bfloat16)}
+    for name, (shape, dtype) in shapes.items():
+        t = bufs.get(name)
+        if t is None or tuple(t.shape) != shape or t.dtype != dtype or t.device != dev:
+            bufs[name] = torch.empty(shape, dtype=dtype, device=dev)
+    need = max(prefill_workspace_bytes(d, seg_len, block_len), 1)
+    ws = bufs.get("workspace")
+    if ws is None or ws.numel() < need or ws.device != dev:
+        bufs["workspace"] = ws = torch.empty((need,), dtype=torch.uint8, device=dev)
+    scale = (1.0 / math.sqrt(D)) if softmax_scale is None else float(softmax_scale)
+    aux = _aux_stream(dev)
+    _check("ei_entropy_guided_prefill",
+           lib().ei_entropy_guided_prefill(
+               _ptr(q), _ptr(k), _ptr(v), d, Tiling(seg_len, block_len), float(probe_scale),
+               budget_params(e_t, alpha, delta_t, base_budget, mult), int(mode), km, scale,
+               _ptr(bufs["log_scores"]), _ptr(bufs["entropy"]), _ptr(bufs["rigid"]),
+               _ptr(bufs["budget"]), _ptr(bufs["idx"]), _ptr(bufs["cnt"]), _ptr(bufs["out"]),
+               _ptr(ws), ws.numel(), _stream(q), ctypes.c_void_p(aux.cuda_stream)))
+    # keep the buffers alive until the auxiliary stream's work has used them
+    for t in list(bufs.values()) + [q, k, v]:
+        if isinstance(t, torch.Tensor):
+            t.record_stream(aux)
+    sel = {n: bufs[n] for n in ("rigid", "budget", "idx", "cnt")}
+    return bufs["out"], sel, bufs["log_scores"], bufs["entropy"]

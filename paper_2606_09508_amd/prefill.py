@@ -3,7 +3,8 @@
 A Llama-3-8B-shaped decoder (random bf16 weights, no checkpoint) runs its
 prefill with the attention of every layer computed by this library: the
 entropy probe, head classification / budgets / top-k selection and the
-block-sparse kernel (``attn="sparse"``), or the dense causal kernel
+block-sparse kernel, in the library's one call that pipelines them over
+KV-head groups (``attn="sparse"``), or the dense causal kernel
 (``attn="dense"``, the full-attention baseline).  Everything around the
 attention is the ordinary decoder layer -- RMSNorm, the Q/K/V/O projections,
 rotary position embedding, the SwiGLU MLP -- on PyTorch (the projections and
@@ -108,33 +109,19 @@ class Attention:
         self.scale = 1.0 / math.sqrt(shape.head_dim)
         self.out = torch.empty((B, shape.n_q_heads, N, shape.head_dim), dtype=torch.bfloat16,
                                device=device)
-        if kind == "sparse":
-            CS, CB = -(-N // cfg.seg_len), -(-N // cfg.block_len)
-            km = eb.kmax(cfg.seg_len, cfg.block_len, cfg.base_budget, cfg.mult)
-            Hq = shape.n_q_heads
-            self.ls = torch.empty((B, Hq, CS, CB), dtype=torch.float32, device=device)
-            self.en = torch.empty((B, Hq, CS), dtype=torch.float32, device=device)
-            dims = eb.Dims(B, Hq, shape.n_kv_heads, N, shape.head_dim)
-            self.ws = torch.empty((eb.probe_workspace_bytes(dims, cfg.seg_len, cfg.block_len),),
-                                  dtype=torch.uint8, device=device)
-            self.sel = {"rigid": torch.empty((B, Hq), dtype=torch.uint8, device=device),
-                        "budget": torch.empty((B, Hq, CS), dtype=torch.int32, device=device),
-                        "idx": torch.empty((B, Hq, CS, km), dtype=torch.int32, device=device),
-                        "cnt": torch.empty((B, Hq, CS), dtype=torch.int32, device=device)}
-        elif kind != "dense":
+        self.bufs = {"out": self.out}   # buffers of the one-call sparse path
+        self.sel = None                  # the last selection (sparse)
+        if kind not in ("sparse", "dense"):
             raise ValueError("attention kind must be 'sparse' or 'dense'")
 
     def __call__(self, q, k, v):
         c = self.cfg
         if self.kind == "dense":
             return eb.dense_prefill_attn(q, k, v, self.scale, True, self.out)
-        N = q.shape[2]
-        eb.entropy_probe(q, k, c.seg_len, c.block_len, c.probe_scale, self.ls, self.en, self.ws)
-        eb.select_blocks(self.ls, self.en, N, c.seg_len, c.block_len, c.entropy_threshold,
-                         c.alpha, c.delta_t, c.base_budget, c.mult,
-                         n_kv_heads=self.shape.n_kv_heads, out=self.sel, mode=c.mode)
-        return eb.sparse_prefill_attn(q, k, v, self.sel["idx"], self.sel["cnt"], c.seg_len,
-                                      c.block_len, self.scale, self.out)
+        o, self.sel, _, _ = eb.entropy_guided_prefill(
+            q, k, v, c.seg_len, c.block_len, c.base_budget, c.entropy_threshold, c.alpha,
+            c.delta_t, c.mult, c.probe_scale, self.scale, bufs=self.bufs, mode=c.mode)
+        return o
 
 
 def layer_forward(x, w, shape: DecoderShape, attn: Attention, cos, sin, trace=None):

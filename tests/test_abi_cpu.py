@@ -35,7 +35,7 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_helpers(L):
-    assert L.ei_abi_version() == 2
+    assert L.ei_abi_version() == 3
     assert eb.kmax(128, 64, 2048, 3) == 98
     assert eb.kmax(2048, 64, 2048, 3) == 96 + 32
     assert eb.kmax(256, 128, 256, 3) == 6 + 2
@@ -52,6 +52,7 @@ def test_helpers(L):
 
 
 FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: every call below fails validation
+FAKE2 = ctypes.c_void_p(0x2000)  # a second fake handle (stream)
 
 
 @pytest.mark.parametrize("dims,tiling,expect", [
@@ -118,3 +119,22 @@ def test_attention_rejects_bad_arguments(L):
     assert L.ei_dense_prefill_attn(FAKE, FAKE, FAKE, eb.Dims(1, 5, 2, 64, 128), 0.088, 1, FAKE,
                                    None) == -2
     assert L.ei_dense_prefill_attn(FAKE, FAKE, FAKE, d, float("nan"), 1, FAKE, None) == -2
+
+
+def test_pipelined_prefill_rejects_bad_arguments(L):
+    d, t = eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(128, 64)
+    p = eb.budget_params(base_budget=256)
+    km = L.ei_kmax(t, p)
+    ws = L.ei_prefill_workspace_bytes(d, t)
+    assert ws > 0 and ws == L.ei_probe_workspace_bytes(eb.Dims(1, 4, 1, 1024, 128), t)
+    outs = (FAKE,) * 7
+    call = L.ei_entropy_guided_prefill
+    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, FAKE, ws, FAKE, None) == -2
+    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, FAKE, ws, FAKE, FAKE) == -2
+    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 5, km, 0.088, *outs, FAKE, ws, FAKE, FAKE2) == -2
+    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km - 1, 0.088, *outs, FAKE, ws, FAKE,
+                FAKE2) == -2
+    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, FAKE, ws - 1, FAKE,
+                FAKE2) == -4
+    assert call(None, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, FAKE, ws, FAKE,
+                FAKE2) == -1

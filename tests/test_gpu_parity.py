@@ -404,3 +404,53 @@ def test_maximum_block_count():
     check_select(w, r)
     amax, amean = check_attention(w, r, _sample_query_rows(w, n=16, seed=8))
     say(f"  entropy rel {hrel:.2e} L {lerr:.2e} attn {amax:.2e}/{amean:.2e}")
+
+
+@pytest.mark.parametrize("case,mode", [
+    (dict(), eb.CLASSIFY_HEAD),
+    (dict(B=2, N=640), eb.CLASSIFY_HEAD),
+    (dict(Hq=7, Hkv=1, N=512), eb.CLASSIFY_GQA_GROUP),
+    (dict(Ls=256, Lb=128, N=1280, base_budget=512), eb.CLASSIFY_SEGMENT),
+    # from 16384 tokens on the call pipelines over KV-head groups on two streams
+    (dict(B=2, Hq=4, Hkv=2, N=16384 + 320), eb.CLASSIFY_HEAD),
+    (dict(Hq=7, Hkv=1, N=16384 + 64), eb.CLASSIFY_GQA_GROUP),
+    (dict(Hq=4, Hkv=2, Ls=256, Lb=128, N=16384 + 384, base_budget=512), eb.CLASSIFY_SEGMENT),
+])
+def test_pipelined_prefill_equals_separate_calls(case, mode):
+    """ei_entropy_guided_prefill gives bitwise the outputs of the three
+    separate calls, below 16384 tokens (one launch per stage on one stream)
+    and above (per KV-head group, probe and select/attention on two streams)."""
+    w = synth.make("c1", 6, **case)
+    q, k, v = to_dev(w.q), to_dev(w.k), to_dev(w.v)
+    ls, en = eb.entropy_probe(q, k, w.Ls, w.Lb, w.probe_scale)
+    sel = eb.select_blocks(ls, en, w.N, w.Ls, w.Lb, w.e_t, w.alpha, w.delta_t, w.base_budget,
+                           w.mult, n_kv_heads=w.Hkv, mode=mode)
+    o = eb.sparse_prefill_attn(q, k, v, sel["idx"], sel["cnt"], w.Ls, w.Lb, w.softmax_scale)
+    o2, sel2, ls2, en2 = eb.entropy_guided_prefill(q, k, v, w.Ls, w.Lb, w.base_budget, w.e_t,
+                                                   w.alpha, w.delta_t, w.mult, w.probe_scale,
+                                                   w.softmax_scale, mode=mode)
+    torch.cuda.synchronize()
+    assert torch.equal(en, en2)
+    r = w.Ls // w.Lb
+    for s in range(w.CS):   # ln A is defined on the visible blocks only
+        nv = min((s + 1) * r, w.CB)
+        assert torch.equal(ls[:, :, s, :nv], ls2[:, :, s, :nv])
+    for name in ("rigid", "budget", "idx", "cnt"):
+        assert torch.equal(sel[name], sel2[name]), name
+    assert torch.equal(o, o2)
+
+
+def test_pipelined_prefill_c2_repeated():
+    """Repeated pipelined calls on a 16k layer with reused buffers stay equal
+    to the separate calls."""
+    w = synth.make("c2", 2, N=16384)
+    q, k, v = to_dev(w.q), to_dev(w.k), to_dev(w.v)
+    ls, en = eb.entropy_probe(q, k, w.Ls, w.Lb)
+    sel = eb.select_blocks(ls, en, w.N, w.Ls, w.Lb, n_kv_heads=w.Hkv)
+    o = eb.sparse_prefill_attn(q, k, v, sel["idx"], sel["cnt"], w.Ls, w.Lb, w.softmax_scale)
+    bufs = {}
+    for _ in range(3):
+        o2, sel2, _, en2 = eb.entropy_guided_prefill(q, k, v, w.Ls, w.Lb, bufs=bufs)
+        torch.cuda.synchronize()
+        assert torch.equal(o, o2) and torch.equal(en, en2)
+        assert torch.equal(sel["idx"], sel2["idx"])
