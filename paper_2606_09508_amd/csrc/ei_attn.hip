@@ -95,15 +95,43 @@ __device__ __forceinline__ void copy16_to_lds(const uint16_t* src, uint32_t lds_
       : "memory");
 }
 
+// The same copy with the global address formed as a wave-uniform base (SGPR
+// pair) plus a 32-bit lane offset, so that issuing it takes no vector
+// arithmetic; M0 is declared clobbered instead of restored.
+__device__ __forceinline__ void copy16_to_lds_s(const unsigned char* sbase, uint32_t voff,
+                                                uint32_t lds_base) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %2"
+      :
+      : "s"(lds_base), "v"(voff), "s"(sbase)
+      : "memory", "m0");
+}
+
 // Global -> LDS without registers: each wave moves 16 rows of K and 16 rows
 // of V (4 + 4 instructions of 64 lanes x 16 bytes).  Lane L of instruction j
-// fills row 16 w + 4 j + L / 16, swizzled chunk position L % 16.  Rows at or
-// past N are read from row N - 1 (finite data whose scores are masked).
+// fills row 16 w + 4 j + L / 16, swizzled chunk position L % 16; koff / voff
+// hold those rows' byte offsets inside a block.  Rows at or past N are read
+// from row N - 1 (finite data whose scores are masked).
 __device__ __forceinline__ void issue_stage(unsigned char* stage, const uint16_t* __restrict__ kh,
                                             const uint16_t* __restrict__ vh, int k0, int N,
-                                            int wave, int lane) {
+                                            int wave, int lane, const uint32_t* koff,
+                                            const uint32_t* voff) {
   const int pos = lane & 15;
   const uint32_t base = (uint32_t)(uintptr_t)stage;
+  if (k0 + kSub <= N) {   // whole block inside the sequence
+    const unsigned char* kb = (const unsigned char*)kh + (size_t)k0 * kRowBytes;
+    const unsigned char* vb = (const unsigned char*)vh + (size_t)k0 * kRowBytes;
+    const uint32_t dst0 =
+        base + (uint32_t)(16 * __builtin_amdgcn_readfirstlane(wave) * kRowBytes);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      copy16_to_lds_s(kb, koff[j], dst0 + 4 * j * kRowBytes);
+      copy16_to_lds_s(vb, voff[j], dst0 + 4 * j * kRowBytes + kTileBytes);
+    }
+    return;
+  }
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int row = 16 * wave + 4 * j + (lane >> 4);
@@ -261,6 +289,15 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(
     return i * kSub;
   };
 
+  // byte offsets of this lane's stage copies inside a 64-row block
+  uint32_t koff[4], voff[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int row = 16 * wave + 4 * j + (lane >> 4);
+    koff[j] = (uint32_t)(row * kRowBytes + 16 * swz(row, lane & 15));
+    voff[j] = (uint32_t)(row * kRowBytes + 16 * swz_v(row, lane & 15));
+  }
+
   f32x16 oacc[4];
 #pragma unroll
   for (int d = 0; d < 4; ++d)
@@ -344,14 +381,14 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(
     }
     if (i + 2 < n_steps) {
       __syncthreads();   // every wave is done reading this stage
-      issue_stage(st, kh, vh, step_key0(i + 2), N, wave, lane);
+      issue_stage(st, kh, vh, step_key0(i + 2), N, wave, lane, koff, voff);
     }
   };
   // Q fragments (and the list) have landed before any stage copy is issued,
   // so no later wait on them covers the copies in flight.
   EI_WAIT_VMCNT(0);
-  if (n_steps > 0) issue_stage(stage0, kh, vh, step_key0(0), N, wave, lane);
-  if (n_steps > 1) issue_stage(stage1, kh, vh, step_key0(1), N, wave, lane);
+  if (n_steps > 0) issue_stage(stage0, kh, vh, step_key0(0), N, wave, lane, koff, voff);
+  if (n_steps > 1) issue_stage(stage1, kh, vh, step_key0(1), N, wave, lane, koff, voff);
   for (int i = 0; i < n_steps; i += 2) {
     step(i, stage0);
     if (i + 1 < n_steps) step(i + 1, stage1);
