@@ -97,16 +97,19 @@ __device__ __forceinline__ void copy16_to_lds(const uint16_t* src, uint32_t lds_
 
 // The same copy with the global address formed as a wave-uniform base (SGPR
 // pair) plus a 32-bit lane offset, so that issuing it takes no vector
-// arithmetic; M0 is declared clobbered instead of restored.
+// arithmetic (M0 restored as above).
 __device__ __forceinline__ void copy16_to_lds_s(const unsigned char* sbase, uint32_t voff,
                                                 uint32_t lds_base) {
+  uint32_t saved;
   asm volatile(
-      "s_mov_b32 m0, %0\n\t"
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
       "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %1, %2"
-      :
+      "global_load_lds_dwordx4 %2, %3\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
       : "s"(lds_base), "v"(voff), "s"(sbase)
-      : "memory", "m0");
+      : "memory");
 }
 
 // Global -> LDS without registers: each wave moves 16 rows of K and 16 rows
