@@ -138,3 +138,25 @@ def test_pipelined_prefill_rejects_bad_arguments(L):
                 FAKE2) == -4
     assert call(None, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, FAKE, ws, FAKE,
                 FAKE2) == -1
+
+
+def test_prefill_workspace_follows_the_two_regimes(L):
+    """Below 16384 tokens the one-call path runs each stage over all heads, so
+    its workspace is the probe workspace of the whole problem; from 16384 on
+    it pipelines over KV-head groups and needs one group's workspace."""
+    t = eb.Tiling(128, 64)
+    short = eb.Dims(2, 32, 8, 8192, 128)
+    assert L.ei_prefill_workspace_bytes(short, t) == L.ei_probe_workspace_bytes(short, t)
+    for n in (16384, 32768, 131072):
+        long_ = eb.Dims(2, 32, 8, n, 128)
+        one = eb.Dims(1, 4, 1, n, 128)
+        assert L.ei_prefill_workspace_bytes(long_, t) == L.ei_probe_workspace_bytes(one, t)
+    # a one-group workspace is too small for a short problem: rejected, nothing launched
+    d = eb.Dims(1, 8, 2, 8192, 128)
+    p = eb.budget_params()
+    km = L.ei_kmax(t, p)
+    ws_one = L.ei_probe_workspace_bytes(eb.Dims(1, 4, 1, 8192, 128), t)
+    assert ws_one < L.ei_prefill_workspace_bytes(d, t)
+    outs = (FAKE,) * 7
+    assert L.ei_entropy_guided_prefill(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, FAKE,
+                                       ws_one, FAKE, FAKE2) == -4
