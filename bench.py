@@ -125,8 +125,8 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: this path shards by KV-head group with no exchange, "
-              "and multi-GPU runs are not part of this build; run with --gpus 1.",
+        print("bench.py measures one GPU: the path shards by KV-head group with no exchange, "
+              "and runs on several GPUs are not implemented; run with --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
 

@@ -68,7 +68,7 @@ const char* ei_status_str(ei_status status) {
     case EI_OK: return "EI_OK";
     case EI_ERR_NULL: return "EI_ERR_NULL: a required pointer is NULL";
     case EI_ERR_SHAPE: return "EI_ERR_SHAPE: inconsistent or out-of-range sizes";
-    case EI_ERR_UNSUPPORTED: return "EI_ERR_UNSUPPORTED: valid but not supported by this build";
+    case EI_ERR_UNSUPPORTED: return "EI_ERR_UNSUPPORTED: valid but not supported by this library";
     case EI_ERR_WORKSPACE: return "EI_ERR_WORKSPACE: workspace missing or too small";
     case EI_ERR_LAUNCH: return "EI_ERR_LAUNCH: a kernel launch failed";
   }
