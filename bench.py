@@ -119,6 +119,10 @@ def main():
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the benchmark line, time the classification variants and "
                          "the L_S / B_h sweeps on the same layer and print a markdown table")
+    ap.add_argument("--et-sweep", action="store_true",
+                    help="instead of the benchmark line, time the path at e_t = 1e-6, 1e-5 and "
+                         "1e-4 and print MFMA utilisation against the computed pair share "
+                         "(meant for --workload c5, the Llama-3-70B layer)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run one device-to-device copy of this size, so that a "
                          "rocprofv3 --pmc run can scale FETCH_SIZE / WRITE_SIZE by it")
@@ -149,6 +153,9 @@ def main():
     q, k, v = to_dev(w.q), to_dev(w.k), to_dev(w.v)
     if args.sweep:
         sweep(args, w, q, k, v)
+        return
+    if args.et_sweep:
+        et_sweep(args, w, q, k, v)
         return
     if args.calibrate_copy_mib > 0:
         n = args.calibrate_copy_mib << 20
@@ -426,6 +433,27 @@ def sweep(args, w, q, k, v):
         print(f"| {name} | {Ls} | {bh} | {int(rigid.sum())}/{w.B * w.Hq} | "
               f"{pairs / dense_pairs:.4f} | {st[0]:.3f} | {st[1]:.3f} | {st[2]:.3f} | {tot:.3f} | "
               f"{4.0 * w.D * pairs / (st[2] * 1e-3) / 1e12:.0f} | {dense_ms / tot:.2f} |",
+              flush=True)
+
+
+def et_sweep(args, w, q, k, v):
+    """Sparse-attention MFMA utilisation against the computed share of the
+    dense pairs for e_t in {1e-6, 1e-5, 1e-4} (markdown table on stdout)."""
+    steps, warmup = max(3, min(args.steps, 10)), max(1, min(args.warmup, 3))
+    dense_pairs = w.B * w.Hq * w.N * (w.N + 1) // 2
+    print(f"Layer: {w.Hq} query / {w.Hkv} KV heads, N = {w.N}, D = {w.D}, L_S = {w.Ls}, "
+          f"L_B = {w.Lb}, B_h = {w.base_budget}, per-head classification, seed {args.seed}; "
+          f"{steps} timed steps after {warmup} warm-up per row.\n")
+    print("| e_t | rigid heads | computed pairs | probe ms | select ms | sparse attn ms "
+          "| sparse TFLOP/s | MFMA util (of 2.5 PFLOP/s) |")
+    print("|---:|---:|---:|---:|---:|---:|---:|---:|")
+    for e_t in (1e-6, 1e-5, 1e-4):
+        st, cnt, idx, rigid = time_path(w, q, k, v, w.Ls, w.Lb, w.base_budget, e_t,
+                                        0, steps, warmup)
+        pairs = causal_pairs(cnt, idx, w.N, w.Ls, w.Lb)
+        tf = 4.0 * w.D * pairs / (st[2] * 1e-3) / 1e12
+        print(f"| {e_t:g} | {int(rigid.sum())}/{w.B * w.Hq} | {pairs / dense_pairs:.4f} | "
+              f"{st[0]:.3f} | {st[1]:.3f} | {st[2]:.3f} | {tf:.0f} | {tf / PEAK_BF16_TFLOPS:.3f} |",
               flush=True)
 
 

@@ -364,6 +364,17 @@ def test_c4_qwen7b_64k_sampled():
     check_select(w, r)
     amax, amean = check_attention(w, r, _sample_query_rows(w, n=48, seed=3))
     say(f"  entropy rel {hrel:.2e} L {lerr:.2e} attn {amax:.2e}/{amean:.2e}")
+    # Retrieval-span recall of the final segment's selection: reported, not a
+    # parity bar (the oracle's selection on the same scores is identical).
+    span_blocks = sorted({j for st, ln in w.spans
+                          for j in range(st // w.Lb, (st + ln - 1) // w.Lb + 1)})
+    idx, cnt = r["sel"]["idx"], r["sel"]["cnt"]
+    s_last = w.CS - 1
+    rec = np.array([[np.isin(span_blocks, idx[b_, h, s_last, :cnt[b_, h, s_last]]).mean()
+                     for h in range(w.Hq)] for b_ in range(w.B)])
+    assert span_blocks and ((rec >= 0) & (rec <= 1)).all()
+    say(f"  span-block recall in the last segment: mean {rec.mean():.3f}, min {rec.min():.3f} "
+        f"over {w.B * w.Hq} heads ({len(span_blocks)} span blocks)")
 
 
 def test_c5_llama70b_128k_sampled():
