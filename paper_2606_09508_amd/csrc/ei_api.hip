@@ -268,7 +268,7 @@ ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const 
   // sa waits for the last work on sb
   if (err == hipSuccess) err = hipEventRecord(ev, sb);
   if (err == hipSuccess) err = hipStreamWaitEvent(sa, ev, 0);
-  hipEventDestroy(ev);   // released once its last record has completed
+  (void)hipEventDestroy(ev);   // released once its last record has completed
   return from_hip(err);
 }
 
