@@ -4,7 +4,8 @@
 //  budget_kernel  one workgroup per (b, query head): the rigid test over all
 //                 segment entropies, the ratios |e_s - e_{s-1}| / e_{s-1} in
 //                 parallel, the clamped budget recurrence (inherently
-//                 sequential, one lane) and k_s = min(floor(B_s / L_B), s r).
+//                 sequential; one wave, increments read across lanes) and
+//                 k_s = min(floor(B_s / L_B), s r).
 //                 Variants: the entropies may be the GQA group's means
 //                 (binary64 sum in head order / G, rounded to binary32), and
 //                 the rigid rule may apply per segment (B_s = B_h wherever
@@ -67,7 +68,7 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(
       ko[s] = (int32_t)min(kb, (int64_t)s * r);
     return;
   }
-  double Bprev = B0;   // meaningful in thread 0 only
+  double Bprev = B0;   // meaningful in wave 0 only
   for (int c0 = 0; c0 < CS; c0 += kChunk) {
     const int n = min(kChunk, CS - c0);
     for (int i = tid; i < n; i += kThreads) {
@@ -86,13 +87,26 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(
       delta[i] = a * t;
     }
     __syncthreads();
-    if (tid == 0) {
-      for (int i = 0; i < n; ++i) {
-        double Bn = Bprev + delta[i];
-        if (!(Bn >= B0)) Bn = B0;
-        if (Bn > cap) Bn = cap;
-        Bs[i] = Bn;
-        Bprev = Bn;
+    if (tid < kWave) {
+      // Wave 0 runs the recurrence 64 segments at a time: lane j holds the
+      // increment of segment i0 + j and each step reads it with v_readlane,
+      // so the dependent chain is the add and the two clamps.  The clamps
+      // as fmax / fmin give the same value as the comparisons in every case
+      // (NaN and -inf -> B_0, +inf -> 3 B_0).  Every lane carries the same
+      // B_prev and writes the same value; past the chunk's end the steps run
+      // on zero increments and their results are not read.
+      for (int i0 = 0; i0 < n; i0 += kWave) {
+        const double dl = tid < n - i0 ? delta[i0 + tid] : 0.0;
+        const uint64_t dbits = __builtin_bit_cast(uint64_t, dl);
+        const int dlo = (int)(uint32_t)dbits, dhi = (int)(uint32_t)(dbits >> 32);
+#pragma unroll
+        for (int j = 0; j < kWave; ++j) {
+          const uint64_t bits =
+              ((uint64_t)(uint32_t)__builtin_amdgcn_readlane(dhi, j) << 32) |
+              (uint64_t)(uint32_t)__builtin_amdgcn_readlane(dlo, j);
+          Bprev = fmin(fmax(Bprev + __builtin_bit_cast(double, bits), B0), cap);
+          Bs[i0 + j] = Bprev;
+        }
       }
     }
     __syncthreads();
