@@ -253,6 +253,34 @@ def test_select_crafted_scores():
             np.testing.assert_array_equal(g[name], ref[name], err_msg=f"{name} B_h={bh}")
 
 
+def test_budget_recurrence_across_chunks():
+    """Alg. 3's recurrence over more segments than one pass of the budget
+    kernel holds (1024): 2085 segments, so B is carried across two chunk
+    boundaries into a ragged last chunk.  Dynamic heads only, with entropy
+    runs that reach both clamps, x / 0 and 0 / 0; budgets, counts and lists
+    bit-exact against the oracle."""
+    Ls, Lb, Hq = 128, 64, 2
+    CS = 2 * 1024 + 37
+    N, CB = CS * Ls, 2 * CS
+    rng = np.random.default_rng(11)
+    en = rng.uniform(0.5, 1.5, (1, Hq, CS)).astype(np.float32)
+    en[0, 0, 1000:1010] = 1.0                    # flat run: the budget decays to B_h
+    en[0, 0, 1020:1030] = [1, 4, 16, 64, 256, 1, 1, 1, 1, 1]   # growth to the 3 B_h cap
+    en[0, 1, 1023:1026] = [0.0, 0.0, 2.0]        # 0 / 0 -> 0, then x / 0 -> inf
+    en[0, 1, 2047:2050] = [0.0, 1.0, 1.0]
+    ls = rng.standard_normal((1, Hq, CS, CB)).astype(np.float32)
+    sel = eb.select_blocks(torch.from_numpy(ls).cuda(), torch.from_numpy(en).cuda(), N, Ls, Lb,
+                           1e-5, 0.5, 0.4, 2048, 3, n_kv_heads=1)
+    torch.cuda.synchronize()
+    g = {kk: t.cpu().numpy() for kk, t in sel.items()}
+    ref = oracle.select(ls, en, N, Ls, Lb, 1e-5, 0.5, 0.4, 2048, 3)
+    assert not ref["rigid"].any()
+    b = ref["budget"][0]
+    assert (b == 32).any() and (b == 96).any() and len(np.unique(b)) > 10
+    for name in ("rigid", "budget", "cnt", "idx"):
+        np.testing.assert_array_equal(g[name], ref[name], err_msg=name)
+
+
 @pytest.mark.parametrize("mode", [eb.CLASSIFY_HEAD, eb.CLASSIFY_GQA_GROUP, eb.CLASSIFY_SEGMENT])
 @pytest.mark.parametrize("e_t", [1e-5, math.inf])
 def test_select_modes_match_oracle(mode, e_t):
