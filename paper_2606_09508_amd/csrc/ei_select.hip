@@ -14,12 +14,14 @@
 //                 recurrence is written, so the result is bit-identical to any
 //                 other IEEE evaluation in that order.
 //  topk_kernel    one wave per (b, h, s) row: the row's past-block scores sit
-//                 in registers as order-preserving 32-bit keys.  The k-th
-//                 largest key T is found by radix selection: an 11-bit
-//                 histogram (in LDS) of the bits below the keys' common prefix
-//                 picks T's bucket; the keys of that bucket (usually few) are
-//                 compacted to one per lane and T's remaining bits are
-//                 resolved there with one ballot per bit.  Ties at T keep the
+//                 in registers as order-preserving 32-bit keys (all loads
+//                 issued before any is used).  The k-th largest key T is
+//                 found by radix selection: an 11-bit histogram (in LDS) of
+//                 the bits below the keys' common prefix picks T's bucket (a
+//                 DPP prefix sum over the lanes' 32-bucket groups, then one
+//                 over the chosen group's buckets); the keys of that bucket
+//                 (usually few) are compacted to one per lane and T's
+//                 remaining bits are resolved there with one ballot per bit.  Ties at T keep the
 //                 highest block indices; the chosen blocks plus the segment's
 //                 own blocks are written ascending.
 #include "../../include/entropyinfer.h"
@@ -133,6 +135,45 @@ constexpr int kWavesPerGroup = kThreads / kWave;
 constexpr int kHistBits = 11;
 constexpr int kHistBins = 1 << kHistBits;
 
+
+// Wave-wide primitives without LDS round trips: DPP within rows of 16 lanes,
+// v_readlane across rows.
+#define EI_DPP_U32(v, ctrl, rmask, bctrl) \
+  ((uint32_t)__builtin_amdgcn_update_dpp(0, (int)(v), (ctrl), (rmask), 0xF, (bctrl)))
+__device__ __forceinline__ uint32_t rl_u32(uint32_t v, int l) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, l);
+}
+__device__ __forceinline__ uint32_t wave_max_u32_f(uint32_t v) {
+  uint32_t t;
+  t = EI_DPP_U32(v, 0xB1, 0xF, false); v = t > v ? t : v;    // quad_perm [1,0,3,2]
+  t = EI_DPP_U32(v, 0x4E, 0xF, false); v = t > v ? t : v;    // quad_perm [2,3,0,1]
+  t = EI_DPP_U32(v, 0x141, 0xF, false); v = t > v ? t : v;   // row_half_mirror
+  t = EI_DPP_U32(v, 0x140, 0xF, false); v = t > v ? t : v;   // row_mirror
+  const uint32_t a = rl_u32(v, 0), b = rl_u32(v, 16), c = rl_u32(v, 32), d = rl_u32(v, 48);
+  const uint32_t ab = a > b ? a : b, cd = c > d ? c : d;
+  return ab > cd ? ab : cd;
+}
+__device__ __forceinline__ uint32_t wave_min_u32_f(uint32_t v) {
+  uint32_t t;
+  t = EI_DPP_U32(v, 0xB1, 0xF, false); v = t < v ? t : v;
+  t = EI_DPP_U32(v, 0x4E, 0xF, false); v = t < v ? t : v;
+  t = EI_DPP_U32(v, 0x141, 0xF, false); v = t < v ? t : v;
+  t = EI_DPP_U32(v, 0x140, 0xF, false); v = t < v ? t : v;
+  const uint32_t a = rl_u32(v, 0), b = rl_u32(v, 16), c = rl_u32(v, 32), d = rl_u32(v, 48);
+  const uint32_t ab = a < b ? a : b, cd = c < d ? c : d;
+  return ab < cd ? ab : cd;
+}
+// Inclusive prefix sum over the 64 lanes (lanes without a source add 0).
+__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t x) {
+  x += EI_DPP_U32(x, 0x111, 0xF, true);   // row_shr:1
+  x += EI_DPP_U32(x, 0x112, 0xF, true);   // row_shr:2
+  x += EI_DPP_U32(x, 0x114, 0xF, true);   // row_shr:4
+  x += EI_DPP_U32(x, 0x118, 0xF, true);   // row_shr:8
+  x += EI_DPP_U32(x, 0x142, 0xA, true);   // row_bcast:15 into rows 1, 3
+  x += EI_DPP_U32(x, 0x143, 0xC, true);   // row_bcast:31 into rows 2, 3
+  return x;
+}
+
 // Order within one wave between its LDS writes and the reads of other lanes.
 __device__ __forceinline__ void wave_lds_fence() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -167,17 +208,22 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
   } else if (kk > 0) {
     uint32_t key[SLOTS];
     uint32_t kmx = 0, kmn = 0xffffffffu;
+    // all loads first, unconditionally (lanes past the row read its last
+    // past block, one shared line), so that they are in flight together
+    float raw[SLOTS];
+#pragma unroll
+    for (int sl = 0; sl < SLOTS; ++sl) raw[sl] = L[min(sl * kWave + lane, npast - 1)];
 #pragma unroll
     for (int sl = 0; sl < SLOTS; ++sl) {
       const int j = sl * kWave + lane;
-      key[sl] = (sl < nsl && j < npast) ? score_key(L[j]) : 0u;
+      key[sl] = (sl < nsl && j < npast) ? score_key(raw[sl]) : 0u;
       if (key[sl]) {
         kmx = key[sl] > kmx ? key[sl] : kmx;
         kmn = key[sl] < kmn ? key[sl] : kmn;
       }
     }
-    kmx = wave_max_u32(kmx);
-    kmn = wave_min_u32(kmn);
+    kmx = wave_max_u32_f(kmx);
+    kmn = wave_min_u32_f(kmn);
     // T = the kk-th largest key; gt / eq = keys above / equal to T.
     uint32_t T;
     int gt = -1, eq = -1;
@@ -200,45 +246,28 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
       wave_lds_fence();
       // Lane l owns buckets 32 l .. 32 l + 31; find the bucket holding T from
       // the top: the largest d with (keys in buckets >= d) >= kk.
-      uint32_t cl[32];
+      uint32_t S = 0;
 #pragma unroll
       for (int qd = 0; qd < 8; ++qd) {
         const uint4 w = ((const uint4*)(hist + 32 * lane))[qd];
-        cl[4 * qd] = w.x;
-        cl[4 * qd + 1] = w.y;
-        cl[4 * qd + 2] = w.z;
-        cl[4 * qd + 3] = w.w;
+        S += (w.x + w.y) + (w.z + w.w);
       }
-      uint32_t S = 0;
-#pragma unroll
-      for (int d = 0; d < 32; ++d) S += cl[d];
-      uint32_t pre = S;   // inclusive prefix over lanes
-#pragma unroll
-      for (int o = 1; o < kWave; o <<= 1) {
-        const uint32_t t = __shfl_up(pre, o);
-        if (lane >= o) pre += t;
-      }
-      const uint32_t total = __shfl(pre, kWave - 1);
+      const uint32_t pre = wave_incl_scan_u32(S);   // inclusive prefix over lanes
+      const uint32_t total = rl_u32(pre, kWave - 1);
       const uint32_t suf = total - pre + S;   // keys in buckets of lanes >= lane
       const uint64_t okm = __ballot(suf >= (uint32_t)kk);
       const int ls = 63 - __clzll(okm);     // okm != 0: total = npast > kk
-      int dstar = 0;
-      uint32_t above = 0;
-      if (lane == ls) {
-        uint32_t acc = suf - S;
-        for (int d = 31; d >= 0; --d) {
-          const uint32_t nacc = acc + cl[d];
-          if (nacc >= (uint32_t)kk) {
-            dstar = 32 * lane + d;
-            above = acc;
-            break;
-          }
-          acc = nacc;
-        }
-      }
-      dstar = __shfl(dstar, ls);
-      above = __shfl(above, ls);
-      const uint32_t nb = hist[dstar];
+      // lane ls's 32 buckets, highest first, one per lane t < 32: T's bucket
+      // is the first at which the keys above ls's buckets plus the running
+      // count reach kk (lane ls itself reaches it, so the ballot is not 0)
+      const uint32_t acc0 = rl_u32(suf - S, ls);
+      const uint32_t bt = lane < 32 ? hist[32 * ls + 31 - lane] : 0u;
+      const uint32_t run = wave_incl_scan_u32(bt);
+      const uint64_t hit = __ballot(lane < 32 && acc0 + run >= (uint32_t)kk);
+      const int tb = (int)__builtin_ctzll(hit);
+      const int dstar = 32 * ls + 31 - tb;
+      const uint32_t above = acc0 + rl_u32(run - bt, tb);
+      const uint32_t nb = rl_u32(bt, tb);
       T = prefix | ((uint32_t)dstar << shift);
       if (shift == 0) {
         gt = (int)above;
