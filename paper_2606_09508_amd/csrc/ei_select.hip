@@ -16,14 +16,15 @@
 //  topk_kernel    one wave per (b, h, s) row: the row's past-block scores sit
 //                 in registers as order-preserving 32-bit keys (all loads
 //                 issued before any is used).  The k-th largest key T is
-//                 found by radix selection: an 11-bit histogram (in LDS) of
-//                 the bits below the keys' common prefix picks T's bucket (a
-//                 DPP prefix sum over the lanes' 32-bucket groups, then one
-//                 over the chosen group's buckets); the keys of that bucket
-//                 (usually few) are compacted to one per lane and T's
-//                 remaining bits are resolved there with one ballot per bit.  Ties at T keep the
-//                 highest block indices; the chosen blocks plus the segment's
-//                 own blocks are written ascending.
+//                 found by radix selection: an 11-bit histogram (in LDS,
+//                 16-bit counters) of the bits below the keys' common prefix
+//                 picks T's bucket (a DPP prefix sum over the lanes' 32-bucket
+//                 groups, then one over the chosen group's buckets); the keys
+//                 of that bucket (usually few) are compacted to one per lane
+//                 and T's remaining bits are resolved there with one ballot
+//                 per bit.  Ties at T keep the highest block indices; the
+//                 chosen blocks plus the segment's own blocks are written
+//                 ascending.
 #include "../../include/entropyinfer.h"
 #include "ei_internal.h"
 
@@ -185,7 +186,8 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
     const float* __restrict__ log_scores, const int32_t* __restrict__ kblocks, int64_t rows,
     int CS, int CB, int r, int kmax, int32_t* __restrict__ idx, int32_t* __restrict__ cnt) {
   // per-wave scratch: bucket counts and the compacted keys of T's bucket
-  __shared__ __attribute__((aligned(16))) uint32_t hist_all[kWavesPerGroup][kHistBins];
+  // bucket counts as 16-bit halves of 32-bit words (a row has at most 8192 keys)
+  __shared__ __attribute__((aligned(16))) uint32_t hist_all[kWavesPerGroup][kHistBins / 2];
   __shared__ uint32_t cand_all[kWavesPerGroup][kWave];
   const int wv = threadIdx.x >> 6;
   const int64_t row = (int64_t)blockIdx.x * kWavesPerGroup + wv;
@@ -238,20 +240,24 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
       const uint32_t prefix = kmx & ~((top == 31) ? 0xffffffffu : ((2u << top) - 1u));
       const int shift = max(top - (kHistBits - 1), 0);
       const uint32_t dmask = (2u << (top - shift)) - 1u;
-      for (int i = lane; i < kHistBins / 4; i += kWave) ((uint4*)hist)[i] = make_uint4(0, 0, 0, 0);
+      for (int i = lane; i < kHistBins / 8; i += kWave) ((uint4*)hist)[i] = make_uint4(0, 0, 0, 0);
       wave_lds_fence();
 #pragma unroll
       for (int sl = 0; sl < SLOTS; ++sl)
-        if (sl < nsl && key[sl]) atomicAdd(&hist[(key[sl] >> shift) & dmask], 1u);
+        if (sl < nsl && key[sl]) {
+          const uint32_t bin = (key[sl] >> shift) & dmask;
+          atomicAdd(&hist[bin >> 1], 1u << (16 * (bin & 1)));
+        }
       wave_lds_fence();
       // Lane l owns buckets 32 l .. 32 l + 31; find the bucket holding T from
       // the top: the largest d with (keys in buckets >= d) >= kk.
-      uint32_t S = 0;
+      uint32_t Sp = 0;   // both halves summed at once: each stays below 2^16
 #pragma unroll
-      for (int qd = 0; qd < 8; ++qd) {
-        const uint4 w = ((const uint4*)(hist + 32 * lane))[qd];
-        S += (w.x + w.y) + (w.z + w.w);
+      for (int qd = 0; qd < 4; ++qd) {
+        const uint4 w = ((const uint4*)(hist + 16 * lane))[qd];
+        Sp += (w.x + w.y) + (w.z + w.w);
       }
+      const uint32_t S = (Sp & 0xffffu) + (Sp >> 16);
       const uint32_t pre = wave_incl_scan_u32(S);   // inclusive prefix over lanes
       const uint32_t total = rl_u32(pre, kWave - 1);
       const uint32_t suf = total - pre + S;   // keys in buckets of lanes >= lane
@@ -261,7 +267,8 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
       // is the first at which the keys above ls's buckets plus the running
       // count reach kk (lane ls itself reaches it, so the ballot is not 0)
       const uint32_t acc0 = rl_u32(suf - S, ls);
-      const uint32_t bt = lane < 32 ? hist[32 * ls + 31 - lane] : 0u;
+      const int bin = 32 * ls + 31 - lane;
+      const uint32_t bt = lane < 32 ? (hist[bin >> 1] >> (16 * (bin & 1))) & 0xffffu : 0u;
       const uint32_t run = wave_incl_scan_u32(bt);
       const uint64_t hit = __ballot(lane < 32 && acc0 + run >= (uint32_t)kk);
       const int tb = (int)__builtin_ctzll(hit);
