@@ -6,6 +6,7 @@ exact (Decimal) evaluation of the definitions and library routines.
 """
 import itertools
 import math
+import os
 from decimal import Decimal, getcontext
 from fractions import Fraction
 
@@ -226,30 +227,52 @@ def test_sampled_rows_equal_full_rows(orc):
 # Algorithm 3: hand-worked sequences (alpha = 0.5, Delta_t = 0.4, e_t = 1e-5)
 # --------------------------------------------------------------------------
 
-# (entropies, rigid, budgets in tokens worked by hand, k = floor(B / 64))
-ALG3_CASES = [
-    # r: -, 0, 1, 0.5, 1, 1e30 -> B: 2048, 1638.4->2048, +614.4, +102.4, +614.4, cap
-    ([1, 1, 2, 1, 1e-30, 1], False, [2048, 2048, 2662.4, 2764.8, 3379.2, 6144],
-     [32, 32, 41, 43, 52, 96]),
-    # r: 0.2 -> clamp; 0.5 -> +102.4; 0 -> -409.6 -> clamp
-    ([0.5, 0.6, 0.9, 0.9, 0.9], False, [2048, 2048, 2150.4, 2048, 2048], [32, 32, 33, 32, 32]),
-    ([1e-6, 1e-6, 1e-6], True, [2048, 2048, 2048], [32, 32, 32]),
-    # 0/0 -> ratio 0; 1/0 -> +inf -> cap; then r = 1: +614.4 above the cap -> cap
-    ([0, 0, 1, 0], False, [2048, 2048, 6144, 6144], [32, 32, 96, 96]),
-    # r = 0.5 -> +102.4; r = 2 -> +1638.4
-    ([2e-5, 1e-5, 3e-5], False, [2048, 2150.4, 3788.8], [32, 33, 59]),
-    # the budget carries over: +614.4, -409.6, -409.6 -> clamp
-    ([1, 2, 2, 2], False, [2048, 2662.4, 2252.8, 2048], [32, 41, 35, 32]),
-    # r = 3 -> +2662.4; r = 3 again -> above 3 B_h -> cap
-    ([1, 4, 16], False, [2048, 4710.4, 6144], [32, 73, 96]),
-    # the maximum must reach e_t for a head to be dynamic: 1e-5 itself is dynamic
-    ([1e-6, 1e-5], False, [2048, 6144], [32, 96]),
-]
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _golden_lines(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return [ln.strip() for ln in f if ln.strip() and not ln.lstrip().startswith("#")]
+
+
+def _alg3_cases():
+    """(entropies, rigid, budgets in tokens worked by hand, k = floor(B / 64))
+    from the golden file."""
+    cases = []
+    for ln in _golden_lines("algorithm3_worked_budgets.txt"):
+        e, rg, Bx, kx = (part.split() for part in ln.split("|"))
+        cases.append(([float(x) for x in e], rg == ["1"], [float(x) for x in Bx],
+                      [int(x) for x in kx]))
+    return cases
+
+
+ALG3_CASES = _alg3_cases()
+ALG3_CONST = {k: float(v) for k, v in (ln.split() for ln in _golden_lines("algorithm3_constants.txt"))}
+
+
+def test_defaults_are_the_papers_constants(orc):
+    """The oracle, the binding and the input generator default to the
+    constants Algorithm 3 and the experimental setup state."""
+    import inspect
+    from paper_2606_09508_amd import binding, synth
+    c = ALG3_CONST
+    want = dict(e_t=c["e_t"], alpha=c["alpha"], delta_t=c["delta_t"],
+                base_budget=c["base_budget_tokens"], mult=c["cap_multiplier"])
+    for fn in (orc.budget, binding.budget_params):
+        d = {k: v.default for k, v in inspect.signature(fn).parameters.items()
+             if v.default is not inspect.Parameter.empty}
+        for k, v in want.items():
+            assert d[k] == v, (fn.__name__, k)
+    w = synth.make("c3", 0, generate_tensors=False)
+    assert (w.e_t, w.alpha, w.delta_t, w.base_budget, w.mult) == \
+        (want["e_t"], want["alpha"], want["delta_t"], want["base_budget"], want["mult"])
 
 
 @pytest.mark.parametrize("e,rigid,Bx,kx", ALG3_CASES)
 def test_algorithm3_worked_sequences(orc, e, rigid, Bx, kx):
-    rg, B = orc.budget(np.asarray(e, np.float32), 1e-5, 0.5, 0.4, 2048, 3)
+    c = ALG3_CONST
+    rg, B = orc.budget(np.asarray(e, np.float32), c["e_t"], c["alpha"], c["delta_t"],
+                       int(c["base_budget_tokens"]), int(c["cap_multiplier"]))
     assert rg == rigid
     np.testing.assert_allclose(B, Bx, rtol=0, atol=2e-3)
     assert [int(math.floor(b / 64)) for b in B] == kx
