@@ -160,3 +160,18 @@ def test_prefill_workspace_follows_the_two_regimes(L):
     outs = (FAKE,) * 7
     assert L.ei_entropy_guided_prefill(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, FAKE,
                                        ws_one, FAKE, FAKE2) == -4
+
+
+def test_bench_refuses_several_gpus():
+    """bench.py measures one GPU: --gpus above 1 (or a multi-rank launch)
+    exits with status 2 and says why, before touching a device."""
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    for extra_env, args in (({}, ["--gpus", "2"]), ({"WORLD_SIZE": "2"}, [])):
+        env = dict(os.environ, **extra_env)
+        r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), *args],
+                           capture_output=True, text=True, timeout=120, env=env, cwd=root)
+        assert r.returncode == 2, (args, extra_env, r.stderr[-500:])
+        assert "one GPU" in (r.stdout + r.stderr)
