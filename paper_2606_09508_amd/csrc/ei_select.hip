@@ -185,8 +185,8 @@ template <int SLOTS>
 __global__ __launch_bounds__(kThreads) void topk_kernel(
     const float* __restrict__ log_scores, const int32_t* __restrict__ kblocks, int64_t rows,
     int CS, int CB, int r, int kmax, int32_t* __restrict__ idx, int32_t* __restrict__ cnt) {
-  // per-wave scratch: bucket counts and the compacted keys of T's bucket
-  // bucket counts as 16-bit halves of 32-bit words (a row has at most 8192 keys)
+  // per-wave scratch: bucket counts (16-bit halves of 32-bit words: a row has
+  // at most 8192 keys) and the compacted keys of T's bucket
   __shared__ __attribute__((aligned(16))) uint32_t hist_all[kWavesPerGroup][kHistBins / 2];
   __shared__ uint32_t cand_all[kWavesPerGroup][kWave];
   const int wv = threadIdx.x >> 6;
@@ -267,7 +267,7 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
       // is the first at which the keys above ls's buckets plus the running
       // count reach kk (lane ls itself reaches it, so the ballot is not 0)
       const uint32_t acc0 = rl_u32(suf - S, ls);
-      const int bin = 32 * ls + 31 - lane;
+      const int bin = 32 * ls + 31 - (lane & 31);
       const uint32_t bt = lane < 32 ? (hist[bin >> 1] >> (16 * (bin & 1))) & 0xffffu : 0u;
       const uint32_t run = wave_incl_scan_u32(bt);
       const uint64_t hit = __ballot(lane < 32 && acc0 + run >= (uint32_t)kk);
