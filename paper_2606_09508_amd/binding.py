@@ -117,6 +117,38 @@ def _req(t: torch.Tensor, name: str, dtype, ndim: int) -> None:
         raise ValueError(f"{name} must be a contiguous {ndim}-d tensor, got {tuple(t.shape)}")
 
 
+def check_qkv_shapes(q_shape, k_shape, v_shape=None) -> None:
+    """q [B, Hq, N, D], k (and v) [B, Hkv, N, D] with Hkv dividing Hq: the C
+    ABI takes every size from q and Hkv, so k / v must match them exactly."""
+    if len(q_shape) != 4 or len(k_shape) != 4:
+        raise ValueError("q and k must be 4-d [B, H, N, D]")
+    B, Hq, N, D = q_shape
+    if (k_shape[0], k_shape[2], k_shape[3]) != (B, N, D):
+        raise ValueError(f"k {tuple(k_shape)} does not match q {tuple(q_shape)} in B, N or D")
+    if k_shape[1] <= 0 or Hq % k_shape[1]:
+        raise ValueError(f"the {k_shape[1]} KV heads must divide the {Hq} query heads")
+    if v_shape is not None and tuple(v_shape) != tuple(k_shape):
+        raise ValueError(f"v {tuple(v_shape)} does not match k {tuple(k_shape)}")
+
+
+def check_score_shapes(ls_shape, en_shape, seq_len: int, seg_len: int, block_len: int) -> None:
+    """log_scores [B, Hq, C_S, C_B] and entropy [B, Hq, C_S] for seq_len
+    tokens: the kernels size every row from seq_len."""
+    CS = -(-seq_len // seg_len) if seg_len > 0 else -1
+    CB = -(-seq_len // block_len) if block_len > 0 else -1
+    if len(ls_shape) != 4 or tuple(ls_shape[2:]) != (CS, CB):
+        raise ValueError(f"log_scores {tuple(ls_shape)} is not [B, Hq, {CS}, {CB}]")
+    if tuple(en_shape) != tuple(ls_shape[:3]):
+        raise ValueError(f"entropy {tuple(en_shape)} is not {tuple(ls_shape[:3])}")
+
+
+def _same_device(*ts) -> None:
+    dev = ts[0].device
+    for t in ts[1:]:
+        if t is not None and t.device != dev:
+            raise ValueError(f"tensors on different devices: {dev} and {t.device}")
+
+
 def dims_of(q: torch.Tensor, k: torch.Tensor) -> Dims:
     B, Hq, N, D = q.shape
     return Dims(B, Hq, k.shape[1], N, D)
@@ -151,6 +183,7 @@ def entropy_probe(q, k, seg_len: int, block_len: int, probe_scale: float = 1.0,
     """ei_entropy_probe: returns (log_scores fp32 [B,Hq,C_S,C_B], entropy fp32 [B,Hq,C_S])."""
     _req(q, "q", torch.bfloat16, 4)
     _req(k, "k", torch.bfloat16, 4)
+    check_qkv_shapes(q.shape, k.shape)
     d = dims_of(q, k)
     CS, CB = num_segments(d.seq_len, seg_len), num_blocks(d.seq_len, block_len)
     dev = q.device
@@ -166,11 +199,13 @@ def entropy_probe(q, k, seg_len: int, block_len: int, probe_scale: float = 1.0,
     need = probe_workspace_bytes(d, seg_len, block_len)
     if workspace is None:
         workspace = torch.empty((max(need, 1),), dtype=torch.uint8, device=dev)
-    _check("ei_entropy_probe",
-           lib().ei_entropy_probe(_ptr(q), _ptr(k), d, Tiling(seg_len, block_len),
-                                  float(probe_scale), _ptr(log_scores), _ptr(entropy),
-                                  _ptr(workspace), workspace.numel() * workspace.element_size(),
-                                  _stream(q)))
+    _same_device(q, k, log_scores, entropy, workspace)
+    with torch.cuda.device(dev):
+        st = lib().ei_entropy_probe(_ptr(q), _ptr(k), d, Tiling(seg_len, block_len),
+                                    float(probe_scale), _ptr(log_scores), _ptr(entropy),
+                                    _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                    _stream(q))
+    _check("ei_entropy_probe", st)
     return log_scores, entropy
 
 
@@ -200,14 +235,19 @@ def select_blocks(log_scores, entropy, seq_len: int, seg_len: int, block_len: in
     _req(out["budget"], "budget", torch.int32, 3)
     _req(out["idx"], "idx", torch.int32, 4)
     _req(out["cnt"], "cnt", torch.int32, 3)
-    if out["idx"].shape[-1] != km:
-        raise ValueError("idx last dimension must equal kmax")
+    check_score_shapes(log_scores.shape, entropy.shape, seq_len, seg_len, block_len)
+    if tuple(out["rigid"].shape) != (B, Hq) or tuple(out["budget"].shape) != (B, Hq, CS) or \
+            tuple(out["idx"].shape) != (B, Hq, CS, km) or tuple(out["cnt"].shape) != (B, Hq, CS):
+        raise ValueError("rigid / budget / idx / cnt do not match [B, Hq], [B, Hq, C_S], "
+                         "[B, Hq, C_S, kmax], [B, Hq, C_S]")
+    _same_device(log_scores, entropy, *out.values())
     d = Dims(B, Hq, Hq if n_kv_heads is None else n_kv_heads, seq_len, head_dim)
-    _check("ei_select_blocks_mode",
-           lib().ei_select_blocks_mode(_ptr(log_scores), _ptr(entropy), d,
-                                       Tiling(seg_len, block_len), p, int(mode), km,
-                                       _ptr(out["rigid"]), _ptr(out["budget"]), _ptr(out["idx"]),
-                                       _ptr(out["cnt"]), _stream(log_scores)))
+    with torch.cuda.device(dev):
+        st = lib().ei_select_blocks_mode(_ptr(log_scores), _ptr(entropy), d,
+                                         Tiling(seg_len, block_len), p, int(mode), km,
+                                         _ptr(out["rigid"]), _ptr(out["budget"]),
+                                         _ptr(out["idx"]), _ptr(out["cnt"]), _stream(log_scores))
+    _check("ei_select_blocks_mode", st)
     return out
 
 
@@ -218,6 +258,7 @@ def sparse_prefill_attn(q, k, v, block_idx, block_cnt, seg_len: int, block_len: 
         _req(t, n, torch.bfloat16, 4)
     _req(block_idx, "block_idx", torch.int32, 4)
     _req(block_cnt, "block_cnt", torch.int32, 3)
+    check_qkv_shapes(q.shape, k.shape, v.shape)
     d = dims_of(q, k)
     if out is None:
         out = torch.empty_like(q)
@@ -229,10 +270,13 @@ def sparse_prefill_attn(q, k, v, block_idx, block_cnt, seg_len: int, block_len: 
             tuple(block_cnt.shape) != (d.batch, d.n_q_heads, CS):
         raise ValueError("block_idx / block_cnt do not match [B, Hq, C_S]")
     sc = 1.0 / math.sqrt(d.head_dim) if softmax_scale is None else float(softmax_scale)
-    _check("ei_sparse_prefill_attn",
-           lib().ei_sparse_prefill_attn(_ptr(q), _ptr(k), _ptr(v), d, Tiling(seg_len, block_len),
-                                        sc, _ptr(block_idx), _ptr(block_cnt),
-                                        int(block_idx.shape[-1]), _ptr(out), _stream(q)))
+    _same_device(q, k, v, block_idx, block_cnt, out)
+    with torch.cuda.device(q.device):
+        st = lib().ei_sparse_prefill_attn(_ptr(q), _ptr(k), _ptr(v), d,
+                                          Tiling(seg_len, block_len), sc, _ptr(block_idx),
+                                          _ptr(block_cnt), int(block_idx.shape[-1]), _ptr(out),
+                                          _stream(q))
+    _check("ei_sparse_prefill_attn", st)
     return out
 
 
@@ -241,6 +285,7 @@ def dense_prefill_attn(q, k, v, softmax_scale: float | None = None, causal: bool
     """ei_dense_prefill_attn: bf16 [B,Hq,N,D] output."""
     for t, n in ((q, "q"), (k, "k"), (v, "v")):
         _req(t, n, torch.bfloat16, 4)
+    check_qkv_shapes(q.shape, k.shape, v.shape)
     d = dims_of(q, k)
     if out is None:
         out = torch.empty_like(q)
@@ -248,9 +293,11 @@ def dense_prefill_attn(q, k, v, softmax_scale: float | None = None, causal: bool
     if k.shape != v.shape or tuple(out.shape) != tuple(q.shape):
         raise ValueError("k / v / out shapes do not match q")
     sc = 1.0 / math.sqrt(d.head_dim) if softmax_scale is None else float(softmax_scale)
-    _check("ei_dense_prefill_attn",
-           lib().ei_dense_prefill_attn(_ptr(q), _ptr(k), _ptr(v), d, sc, 1 if causal else 0,
-                                       _ptr(out), _stream(q)))
+    _same_device(q, k, v, out)
+    with torch.cuda.device(q.device):
+        st = lib().ei_dense_prefill_attn(_ptr(q), _ptr(k), _ptr(v), d, sc, 1 if causal else 0,
+                                         _ptr(out), _stream(q))
+    _check("ei_dense_prefill_attn", st)
     return out
 
 
@@ -281,6 +328,8 @@ def entropy_guided_prefill(q, k, v, seg_len: int = 128, block_len: int = 64,
     entropy)."""
     for t, n in ((q, "q"), (k, "k"), (v, "v")):
         _req(t, n, torch.bfloat16, 4)
+    check_qkv_shapes(q.shape, k.shape, v.shape)
+    _same_device(q, k, v)
     d = dims_of(q, k)
     B, Hq, N, D = q.shape
     CS, CB = num_segments(N, seg_len), num_blocks(N, block_len)
@@ -301,13 +350,14 @@ def entropy_guided_prefill(q, k, v, seg_len: int = 128, block_len: int = 64,
         bufs["workspace"] = ws = torch.empty((need,), dtype=torch.uint8, device=dev)
     scale = (1.0 / math.sqrt(D)) if softmax_scale is None else float(softmax_scale)
     aux = _aux_stream(dev)
-    _check("ei_entropy_guided_prefill",
-           lib().ei_entropy_guided_prefill(
-               _ptr(q), _ptr(k), _ptr(v), d, Tiling(seg_len, block_len), float(probe_scale),
-               budget_params(e_t, alpha, delta_t, base_budget, mult), int(mode), km, scale,
-               _ptr(bufs["log_scores"]), _ptr(bufs["entropy"]), _ptr(bufs["rigid"]),
-               _ptr(bufs["budget"]), _ptr(bufs["idx"]), _ptr(bufs["cnt"]), _ptr(bufs["out"]),
-               _ptr(ws), ws.numel(), _stream(q), ctypes.c_void_p(aux.cuda_stream)))
+    with torch.cuda.device(dev):
+        st = lib().ei_entropy_guided_prefill(
+            _ptr(q), _ptr(k), _ptr(v), d, Tiling(seg_len, block_len), float(probe_scale),
+            budget_params(e_t, alpha, delta_t, base_budget, mult), int(mode), km, scale,
+            _ptr(bufs["log_scores"]), _ptr(bufs["entropy"]), _ptr(bufs["rigid"]),
+            _ptr(bufs["budget"]), _ptr(bufs["idx"]), _ptr(bufs["cnt"]), _ptr(bufs["out"]),
+            _ptr(ws), ws.numel(), _stream(q), ctypes.c_void_p(aux.cuda_stream))
+    _check("ei_entropy_guided_prefill", st)
     # keep the buffers alive until the auxiliary stream's work has used them
     for t in list(bufs.values()) + [q, k, v]:
         if isinstance(t, torch.Tensor):

@@ -175,3 +175,25 @@ def test_bench_refuses_several_gpus():
                            capture_output=True, text=True, timeout=120, env=env, cwd=root)
         assert r.returncode == 2, (args, extra_env, r.stderr[-500:])
         assert "one GPU" in (r.stdout + r.stderr)
+
+
+def test_binding_shape_checks():
+    """The binding refuses tensors whose sizes differ from what the C ABI
+    derives from q's shape and seq_len (a kernel would read past them)."""
+    import pytest
+    from paper_2606_09508_amd import binding as eb
+    q = (1, 4, 128, 128)
+    eb.check_qkv_shapes(q, (1, 2, 128, 128), (1, 2, 128, 128))
+    for kb in [(2, 2, 128, 128), (1, 2, 64, 128), (1, 2, 128, 64), (1, 3, 128, 128),
+               (1, 0, 128, 128), (1, 2, 128)]:
+        with pytest.raises(ValueError):
+            eb.check_qkv_shapes(q, kb)
+    with pytest.raises(ValueError):
+        eb.check_qkv_shapes(q, (1, 2, 128, 128), (1, 2, 127, 128))
+    eb.check_score_shapes((1, 4, 8, 16), (1, 4, 8), 1024, 128, 64)
+    eb.check_score_shapes((2, 4, 8, 16), (2, 4, 8), 1000, 128, 64)     # ragged tail
+    for ls, en, n in [((1, 4, 8, 15), (1, 4, 8), 1024), ((1, 4, 8, 16), (1, 4, 7), 1024),
+                      ((1, 4, 8, 16), (1, 4, 8), 1100), ((1, 4, 8, 16), (2, 4, 8), 1024),
+                      ((4, 8, 16), (4, 8), 1024)]:
+        with pytest.raises(ValueError):
+            eb.check_score_shapes(ls, en, n, 128, 64)

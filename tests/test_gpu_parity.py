@@ -181,6 +181,22 @@ def test_deterministic():
     assert torch.equal(a["o"], b["o"])
 
 
+def test_binding_refuses_mismatched_tensors():
+    """k / v / score tensors that do not match q's sizes raise before any launch."""
+    w = synth.make("c1", 4, N=512)
+    q, k, v = to_dev(w.q), to_dev(w.k), to_dev(w.v)
+    with pytest.raises(ValueError):
+        eb.dense_prefill_attn(q, k[:, :, :256].contiguous(), v[:, :, :256].contiguous())
+    with pytest.raises(ValueError):
+        eb.entropy_probe(q, k[:, :, :256].contiguous(), w.Ls, w.Lb)
+    ls, en = eb.entropy_probe(q, k, w.Ls, w.Lb, w.probe_scale)
+    with pytest.raises(ValueError):
+        eb.select_blocks(ls, en, 2 * w.N, w.Ls, w.Lb, n_kv_heads=w.Hkv)
+    with pytest.raises(ValueError):
+        eb.select_blocks(ls[:, :, :, :-1].contiguous(), en, w.N, w.Ls, w.Lb, n_kv_heads=w.Hkv)
+    torch.cuda.synchronize()
+
+
 def test_malformed_block_list_is_safe():
     """Out-of-range, descending and oversized counts stop the list walk."""
     w = synth.make("c1", 4, N=512)
