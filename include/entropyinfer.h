@@ -27,9 +27,14 @@
  *  - Every argument is validated on the host before anything is launched; a
  *    failed check returns a negative ei_status and launches nothing.
  *    B == 0 or N == 0 is valid and launches nothing.
+ *  - Alignment: bf16 tensors (Q, K, V, O) and workspaces start on a 16-byte
+ *    boundary, fp32 / int32 arrays on a 4-byte one (hipMalloc returns
+ *    256-byte aligned memory); a pointer that is not returns
+ *    EI_ERR_UNSUPPORTED.
  *  - Outputs must not alias inputs.  Identical inputs give bitwise-identical
- *    outputs (no atomics in any reduction).  No global state, no logging;
- *    calls on different streams may run concurrently.
+ *    outputs (the only atomics are integer counts in LDS, whose order does
+ *    not matter).  No global state, no logging; calls on different streams
+ *    may run concurrently.
  */
 #ifndef ENTROPYINFER_H
 #define ENTROPYINFER_H
@@ -45,7 +50,8 @@ typedef enum {
   EI_OK = 0,
   EI_ERR_NULL = -1,        /* a required pointer is NULL */
   EI_ERR_SHAPE = -2,       /* inconsistent or out-of-range sizes */
-  EI_ERR_UNSUPPORTED = -3, /* valid but not implemented here (e.g. D != 128) */
+  EI_ERR_UNSUPPORTED = -3, /* valid but not implemented here (e.g. D != 128,
+                              a misaligned pointer) */
   EI_ERR_WORKSPACE = -4,   /* workspace missing or smaller than required */
   EI_ERR_LAUNCH = -5       /* a kernel launch failed (hipGetLastError) */
 } ei_status;

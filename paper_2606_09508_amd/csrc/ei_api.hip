@@ -6,6 +6,8 @@
 
 #include <limits.h>
 
+#include <initializer_list>
+
 namespace {
 
 constexpr int32_t kAbiVersion = 3;
@@ -56,6 +58,20 @@ int32_t kmax_of(const ei_tiling& t, const ei_budget_params& p) {
 }
 
 ei_status from_hip(hipError_t e) { return e == hipSuccess ? EI_OK : EI_ERR_LAUNCH; }
+
+// The kernels move bf16 tensors and the workspace in 16-byte vectors (and by
+// LDS DMA), fp32 / int32 arrays in 4-byte words.
+bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+bool aligned16(std::initializer_list<const void*> ps) {
+  for (const void* p : ps)
+    if (!aligned(p, 16)) return false;
+  return true;
+}
+bool aligned4(std::initializer_list<const void*> ps) {
+  for (const void* p : ps)
+    if (!aligned(p, 4)) return false;
+  return true;
+}
 
 }  // namespace
 
@@ -108,11 +124,13 @@ ei_status ei_entropy_probe(const uint16_t* q, const uint16_t* k, ei_dims dims, e
   const Sizes z = sizes(dims, &tiling);
   if (z.B == 0 || z.N == 0) return EI_OK;
   if (!q || !k || !log_scores || !entropy) return EI_ERR_NULL;
+  if (!aligned16({q, k}) || !aligned4({log_scores, entropy})) return EI_ERR_UNSUPPORTED;
   const ei::ProbeShape ps{(int)z.B, (int)z.Hq, (int)z.Hkv, (int)z.N, tiling.seg_len,
                           tiling.block_len, (int)z.CS, (int)z.CB, (int)z.r};
   if (!ei::probe_supported(ps)) return EI_ERR_UNSUPPORTED;
   if (!workspace || workspace_bytes < ei::probe_qrep_bytes(ps) + ei::probe_krep_bytes(ps))
     return EI_ERR_WORKSPACE;
+  if (!aligned16({workspace})) return EI_ERR_UNSUPPORTED;
   return from_hip(ei::launch_probe(q, k, ps, probe_scale, log_scores, entropy, workspace,
                                    (hipStream_t)stream));
 }
@@ -139,6 +157,8 @@ ei_status ei_select_blocks_mode(const float* log_scores, const float* entropy, e
   if (z.B == 0 || z.N == 0) return EI_OK;
   if (!log_scores || !entropy || !head_is_rigid || !budget_blocks || !block_idx || !block_cnt)
     return EI_ERR_NULL;
+  if (!aligned4({log_scores, entropy, budget_blocks, block_idx, block_cnt}))
+    return EI_ERR_UNSUPPORTED;
   const ei::SelectShape ss{(int)z.B, (int)z.Hq, (int)z.N, tiling.seg_len, tiling.block_len,
                            (int)z.CS, (int)z.CB, (int)z.r, kmax, params.entropy_threshold,
                            params.alpha, params.delta_t, params.base_budget_tokens,
@@ -159,6 +179,7 @@ ei_status ei_sparse_prefill_attn(const uint16_t* q, const uint16_t* k, const uin
   const Sizes z = sizes(dims, &tiling);
   if (z.B == 0 || z.N == 0) return EI_OK;
   if (!q || !k || !v || !block_idx || !block_cnt || !o) return EI_ERR_NULL;
+  if (!aligned16({q, k, v, o}) || !aligned4({block_idx, block_cnt})) return EI_ERR_UNSUPPORTED;
   const ei::AttnShape as{(int)z.B, (int)z.Hq, (int)z.Hkv, (int)z.N, tiling.seg_len,
                          tiling.block_len, (int)z.CS, (int)z.CB, kmax, softmax_scale};
   return from_hip(ei::launch_attention(q, k, v, as, ei::kSparse, block_idx, block_cnt, o,
@@ -198,6 +219,9 @@ ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const 
   if (!q || !k || !v || !log_scores || !entropy || !head_is_rigid || !budget_blocks ||
       !block_idx || !block_cnt || !o)
     return EI_ERR_NULL;
+  if (!aligned16({q, k, v, o}) ||
+      !aligned4({log_scores, entropy, budget_blocks, block_idx, block_cnt}))
+    return EI_ERR_UNSUPPORTED;
   const int G = (int)(z.Hq / z.Hkv);
   // Short sequences: the per-group launches cost more than the overlap saves;
   // run the three stages over all heads on `stream` (the workspace then
@@ -211,6 +235,7 @@ ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const 
   if (!ei::probe_supported(pw)) return EI_ERR_UNSUPPORTED;
   if (!workspace || workspace_bytes < ei::probe_qrep_bytes(pw) + ei::probe_krep_bytes(pw))
     return EI_ERR_WORKSPACE;
+  if (!aligned16({workspace})) return EI_ERR_UNSUPPORTED;
   const ei::SelectShape ss{1, G, (int)z.N, tiling.seg_len, tiling.block_len, (int)z.CS,
                            (int)z.CB, (int)z.r, kmax, params.entropy_threshold, params.alpha,
                            params.delta_t, params.base_budget_tokens, params.max_budget_mult,
@@ -281,6 +306,7 @@ ei_status ei_dense_prefill_attn(const uint16_t* q, const uint16_t* k, const uint
   const Sizes z = sizes(dims, nullptr);
   if (z.B == 0 || z.N == 0) return EI_OK;
   if (!q || !k || !v || !o) return EI_ERR_NULL;
+  if (!aligned16({q, k, v, o})) return EI_ERR_UNSUPPORTED;
   const ei::AttnShape as{(int)z.B, (int)z.Hq, (int)z.Hkv, (int)z.N, 128, 64, 0, 0, 0,
                          softmax_scale};
   return from_hip(ei::launch_attention(q, k, v, as,

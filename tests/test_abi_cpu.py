@@ -197,3 +197,41 @@ def test_binding_shape_checks():
                       ((4, 8, 16), (4, 8), 1024)]:
         with pytest.raises(ValueError):
             eb.check_score_shapes(ls, en, n, 128, 64)
+
+
+def _off(p, n):
+    return ctypes.c_void_p(p.value + n)
+
+
+def test_misaligned_pointers_are_refused(L):
+    """bf16 tensors and workspaces need 16-byte, fp32 / int32 arrays 4-byte
+    alignment; anything else returns EI_ERR_UNSUPPORTED before a launch."""
+    d, t = eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(128, 64)
+    need = L.ei_probe_workspace_bytes(d, t)
+    probe = L.ei_entropy_probe
+    assert probe(_off(FAKE, 2), FAKE, d, t, 1.0, FAKE, FAKE, FAKE, need, None) == -3
+    assert probe(FAKE, _off(FAKE, 8), d, t, 1.0, FAKE, FAKE, FAKE, need, None) == -3
+    assert probe(FAKE, FAKE, d, t, 1.0, _off(FAKE, 2), FAKE, FAKE, need, None) == -3
+    assert probe(FAKE, FAKE, d, t, 1.0, FAKE, FAKE, _off(FAKE, 8), need, None) == -3
+    p = eb.budget_params(base_budget=256)
+    km = L.ei_kmax(t, p)
+    sel = L.ei_select_blocks
+    assert sel(_off(FAKE, 2), FAKE, d, t, p, km, FAKE, FAKE, FAKE, FAKE, None) == -3
+    assert sel(FAKE, FAKE, d, t, p, km, FAKE, FAKE, _off(FAKE, 1), FAKE, None) == -3
+    assert sel(FAKE, FAKE, d, t, p, km, _off(FAKE, 1), FAKE, FAKE, _off(FAKE, 3), None) == -3
+    spa = L.ei_sparse_prefill_attn
+    assert spa(FAKE, FAKE, _off(FAKE, 8), d, t, 0.088, FAKE, FAKE, km, FAKE, None) == -3
+    assert spa(FAKE, FAKE, FAKE, d, t, 0.088, FAKE, FAKE, km, _off(FAKE, 4), None) == -3
+    assert spa(FAKE, FAKE, FAKE, d, t, 0.088, _off(FAKE, 2), FAKE, km, FAKE, None) == -3
+    assert L.ei_dense_prefill_attn(FAKE, _off(FAKE, 2), FAKE, d, 0.088, 1, FAKE, None) == -3
+    assert L.ei_dense_prefill_attn(FAKE, FAKE, FAKE, d, 0.088, 0, _off(FAKE, 8), None) == -3
+    ws = L.ei_prefill_workspace_bytes(d, t)
+    call = L.ei_entropy_guided_prefill
+    outs = [FAKE] * 7
+    assert call(FAKE, FAKE, _off(FAKE, 2), d, t, 1.0, p, 0, km, 0.088, *outs, FAKE, ws, FAKE,
+                FAKE2) == -3
+    bad = list(outs)
+    bad[4] = _off(FAKE, 2)   # block_idx
+    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *bad, FAKE, ws, FAKE, FAKE2) == -3
+    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, _off(FAKE, 8), ws, FAKE,
+                FAKE2) == -3
