@@ -57,7 +57,8 @@ typedef enum {
 } ei_status;
 
 /* Problem sizes: batch B, query heads Hq, key/value heads Hkv, sequence N,
- * head dimension D. */
+ * head dimension D.  Every launch's grid is bounded by B * Hq * ceil(N / 128)
+ * workgroups, which must not exceed 2^31 - 1 (else EI_ERR_SHAPE). */
 typedef struct {
   int32_t batch, n_q_heads, n_kv_heads, seq_len, head_dim;
 } ei_dims;

@@ -25,6 +25,10 @@ ei_status check_dims(const ei_dims& d) {
   if (d.n_q_heads % d.n_kv_heads) return EI_ERR_SHAPE;
   // element offsets are formed in 64-bit, (batch, head) indices in 32-bit
   if ((int64_t)d.batch * d.n_q_heads > INT_MAX / 2) return EI_ERR_SHAPE;
+  // every grid (workgroups per (batch, head, 128-row tile or segment)) fits
+  // in 31 bits
+  if ((int64_t)d.batch * d.n_q_heads * (((int64_t)d.seq_len + 127) / 128) > INT_MAX)
+    return EI_ERR_SHAPE;
   if (d.head_dim != ei::kHeadDim) return EI_ERR_UNSUPPORTED;
   return EI_OK;
 }

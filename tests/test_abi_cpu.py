@@ -235,3 +235,18 @@ def test_misaligned_pointers_are_refused(L):
     assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *bad, FAKE, ws, FAKE, FAKE2) == -3
     assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, _off(FAKE, 8), ws, FAKE,
                 FAKE2) == -3
+
+
+def test_sizes_whose_grids_overflow_are_refused(L):
+    """B x Hq x ceil(N / 128) workgroups must fit in 31 bits (every launch's
+    grid is bounded by it): larger problems are EI_ERR_SHAPE on the host."""
+    t = eb.Tiling(128, 64)
+    big = eb.Dims(1, 1 << 20, 1 << 10, 1 << 20, 128)      # 2^20 heads x 2^13 tiles
+    assert L.ei_num_segments(big, t) == -1
+    assert L.ei_probe_workspace_bytes(big, t) == 0
+    assert L.ei_entropy_probe(FAKE, FAKE, big, t, 1.0, FAKE, FAKE, FAKE, 1 << 30, None) == -2
+    assert L.ei_dense_prefill_attn(FAKE, FAKE, FAKE, big, 0.088, 1, FAKE, None) == -2
+    assert L.ei_sparse_prefill_attn(FAKE, FAKE, FAKE, big, t, 0.088, FAKE, FAKE, 98, FAKE,
+                                    None) == -2
+    ok = eb.Dims(1, 1 << 17, 1 << 10, 1 << 20, 128)       # 2^17 x 2^13 = 2^30 workgroups
+    assert L.ei_num_segments(ok, t) == (1 << 20) // 128
