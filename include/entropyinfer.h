@@ -8,7 +8,8 @@
  *                           per-segment top-k key-block selection (Section 4.2,
  *                           Appendix A Eq. t_topk)
  *   ei_sparse_prefill_attn  causal GQA attention over the selected blocks
- *                           (Appendix A Eq. t_spa)
+ *                           (Appendix A Eq. t_spa); _gqa_union: the same with
+ *                           two query heads of a KV group per tile
  *   ei_dense_prefill_attn   dense (causal) GQA attention, the full-attention
  *                           baseline the paper compares against
  *
@@ -211,6 +212,25 @@ ei_status ei_sparse_prefill_attn(const uint16_t* q, const uint16_t* k, const uin
                                  ei_dims dims, ei_tiling tiling, float softmax_scale,
                                  const int32_t* block_idx, const int32_t* block_cnt,
                                  int32_t kmax, uint16_t* o, void* stream);
+
+/*
+ * ei_sparse_prefill_attn_gqa_union -- the same attention as
+ * ei_sparse_prefill_attn with GQA-union tiles (Section 5's end-to-end latency
+ * study puts the method's extra cost over uniform budgets on its per-head
+ * budgets, whose heads no longer share K/V loads): one workgroup takes a
+ * query tile of two query heads of the same KV head,
+ * copies each block of the union of their lists once and lets each head
+ * compute only its own blocks.  Same arguments and bitwise the same output as
+ * ei_sparse_prefill_attn.
+ *
+ * Errors: as ei_sparse_prefill_attn; EI_ERR_UNSUPPORTED also when
+ * kmax > 128 or C_B > 8192 (the merged list lives in LDS).
+ */
+ei_status ei_sparse_prefill_attn_gqa_union(const uint16_t* q, const uint16_t* k,
+                                           const uint16_t* v, ei_dims dims, ei_tiling tiling,
+                                           float softmax_scale, const int32_t* block_idx,
+                                           const int32_t* block_cnt, int32_t kmax, uint16_t* o,
+                                           void* stream);
 
 /*
  * ei_dense_prefill_attn -- dense GQA attention (Section 2's A_h V), causal

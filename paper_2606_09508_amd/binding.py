@@ -86,6 +86,8 @@ def lib() -> ctypes.CDLL:
                                                 BudgetParams, ctypes.c_int32, ctypes.c_int32,
                                                 ctypes.c_float, _VP, _VP, _VP, _VP, _VP, _VP,
                                                 _VP, _VP, ctypes.c_size_t, _VP, _VP]
+        L.ei_sparse_prefill_attn_gqa_union.restype = ctypes.c_int
+        L.ei_sparse_prefill_attn_gqa_union.argtypes = L.ei_sparse_prefill_attn.argtypes
         L.ei_dense_prefill_attn.restype = ctypes.c_int
         L.ei_dense_prefill_attn.argtypes = [_VP, _VP, _VP, Dims, ctypes.c_float, ctypes.c_int32,
                                             _VP, _VP]
@@ -252,8 +254,9 @@ def select_blocks(log_scores, entropy, seq_len: int, seg_len: int, block_len: in
 
 
 def sparse_prefill_attn(q, k, v, block_idx, block_cnt, seg_len: int, block_len: int,
-                        softmax_scale: float | None = None, out=None):
-    """ei_sparse_prefill_attn: bf16 [B,Hq,N,D] output."""
+                        softmax_scale: float | None = None, out=None, gqa_union: bool = False):
+    """ei_sparse_prefill_attn (or, with gqa_union, ei_sparse_prefill_attn_gqa_union,
+    bitwise the same result): bf16 [B,Hq,N,D] output."""
     for t, n in ((q, "q"), (k, "k"), (v, "v")):
         _req(t, n, torch.bfloat16, 4)
     _req(block_idx, "block_idx", torch.int32, 4)
@@ -272,11 +275,11 @@ def sparse_prefill_attn(q, k, v, block_idx, block_cnt, seg_len: int, block_len: 
     sc = 1.0 / math.sqrt(d.head_dim) if softmax_scale is None else float(softmax_scale)
     _same_device(q, k, v, block_idx, block_cnt, out)
     with torch.cuda.device(q.device):
-        st = lib().ei_sparse_prefill_attn(_ptr(q), _ptr(k), _ptr(v), d,
-                                          Tiling(seg_len, block_len), sc, _ptr(block_idx),
-                                          _ptr(block_cnt), int(block_idx.shape[-1]), _ptr(out),
-                                          _stream(q))
-    _check("ei_sparse_prefill_attn", st)
+        fn = "ei_sparse_prefill_attn_gqa_union" if gqa_union else "ei_sparse_prefill_attn"
+        st = getattr(lib(), fn)(_ptr(q), _ptr(k), _ptr(v), d, Tiling(seg_len, block_len), sc,
+                                _ptr(block_idx), _ptr(block_cnt), int(block_idx.shape[-1]),
+                                _ptr(out), _stream(q))
+    _check(fn, st)
     return out
 
 

@@ -190,6 +190,26 @@ ei_status ei_sparse_prefill_attn(const uint16_t* q, const uint16_t* k, const uin
                                        (hipStream_t)stream));
 }
 
+ei_status ei_sparse_prefill_attn_gqa_union(const uint16_t* q, const uint16_t* k,
+                                           const uint16_t* v, ei_dims dims, ei_tiling tiling,
+                                           float softmax_scale, const int32_t* block_idx,
+                                           const int32_t* block_cnt, int32_t kmax, uint16_t* o,
+                                           void* stream) {
+  ei_status st = check_dims(dims);
+  if (st != EI_OK) return st;
+  if ((st = check_tiling(tiling)) != EI_OK) return st;
+  if (kmax <= 0 || !(softmax_scale == softmax_scale)) return EI_ERR_SHAPE;
+  const Sizes z = sizes(dims, &tiling);
+  if (z.B == 0 || z.N == 0) return EI_OK;
+  if (!q || !k || !v || !block_idx || !block_cnt || !o) return EI_ERR_NULL;
+  if (!aligned16({q, k, v, o}) || !aligned4({block_idx, block_cnt})) return EI_ERR_UNSUPPORTED;
+  const ei::AttnShape as{(int)z.B, (int)z.Hq, (int)z.Hkv, (int)z.N, tiling.seg_len,
+                         tiling.block_len, (int)z.CS, (int)z.CB, kmax, softmax_scale};
+  if (!ei::attention_union_supported(as)) return EI_ERR_UNSUPPORTED;
+  return from_hip(ei::launch_attention_union(q, k, v, as, block_idx, block_cnt, o,
+                                             (hipStream_t)stream));
+}
+
 size_t ei_prefill_workspace_bytes(ei_dims dims, ei_tiling tiling) {
   if (check_dims(dims) != EI_OK || check_tiling(tiling) != EI_OK) return 0;
   // short sequences: one probe over all heads

@@ -182,6 +182,120 @@ __device__ __forceinline__ bf16x8 read_vt(const unsigned char* stage, int dt, in
 // the exact softmax.
 constexpr float kRescaleThreshold = 8.0f;
 
+// Valid prefix of a block list of c entries, 64 at a time: strictly
+// ascending, inside [0, C_B), and not wholly after the tile's last query.
+template <int SUB>
+__device__ __forceinline__ int valid_prefix(const int32_t* lst, int c, int CB, int q_last,
+                                            int lane) {
+  int nv = 0;
+  for (int base = 0; base < c; base += kWave) {
+    const int e = base + lane;
+    bool ok = false;
+    if (e < c) {
+      const int blk = lst[e];
+      const int prv = e > 0 ? lst[e - 1] : -1;
+      ok = blk > prv && blk < CB && blk * SUB * kSub <= q_last;
+    }
+    const uint64_t bad = ~__builtin_amdgcn_ballot_w64(ok);
+    if (bad != 0) {
+      nv = base + (int)__builtin_ctzll(bad);
+      break;
+    }
+    nv = base + kWave;
+  }
+  return min(nv, c);
+}
+
+// One 64-key sub-block (staged at st, first key k0) for the wave's 32 query
+// rows: S^T = K Q^T, the causal / length mask, the online softmax with lazy
+// rescaling, and O^T += V^T P^T.
+template <int MODE>
+__device__ __forceinline__ void compute_step(const unsigned char* st, int k0, int qw0, int qrow,
+                                             int N, int jq, int hf, int lane, const bf16x8* qf,
+                                             float sc_log2, f32x16* oacc, float& m_i,
+                                             float& l_i) {
+  // S^T = K Q^T for the 64 keys (two 32-key tiles).
+  f32x16 sacc[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sacc[u][r] = 0.0f;
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+      sacc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(read_k(st, 32 * u + jq, s, hf), qf[s],
+                                                       sacc[u], 0, 0, 0);
+  }
+  // mask keys after the query (causal) or at / past N; branch-free
+  const bool need_mask = (MODE != kDenseFull && k0 + kSub - 1 > qw0) || (k0 + kSub > N);
+  if (need_mask) {
+    const int lim = (MODE == kDenseFull ? N - 1 : min(qrow, N - 1)) - k0 - 4 * hf;
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int kk = 32 * u + 8 * (r >> 2) + (r & 3);
+        sacc[u][r] = (kk <= lim) ? sacc[u][r] : -INFINITY;
+      }
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[u][r]);
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  const float mcand = mx * sc_log2;
+  if (__builtin_amdgcn_ballot_w64(mcand > m_i + kRescaleThreshold) != 0) {
+    const float m_new = fmaxf(m_i, mcand);
+    const float alpha = (m_new == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f(m_i - m_new);
+    l_i *= alpha;
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[d][r] *= alpha;
+    m_i = m_new;
+  }
+  const float mneg = (m_i == -INFINITY) ? 0.0f : -m_i;
+  uint4 pw[4];   // P^T as bf16, one 16-key MFMA step each
+  float lsum = 0.0f;
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    const int u = s >> 1, base = 8 * (s & 1);
+    float p[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      p[e] = __builtin_amdgcn_exp2f(fmaf(sacc[u][base + e], sc_log2, mneg));
+      lsum += p[e];
+    }
+    pw[s] = make_uint4(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
+                       pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7]));
+  }
+  l_i += lsum;
+  // O^T += V^T P^T
+#pragma unroll
+  for (int d = 0; d < 4; ++d)
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(read_vt(st, d, s, lane), as_bf16x8(pw[s]),
+                                                       oacc[d], 0, 0, 0);
+}
+
+// O = O^T / l for the lane's query row, bf16.
+__device__ __forceinline__ void store_rows(uint16_t* __restrict__ o, size_t row_base, int hf,
+                                           const f32x16* oacc, float l_i) {
+  const float l = l_i + __shfl_xor(l_i, 32);
+  const float inv = l > 0.0f ? 1.0f / l : 0.0f;
+  uint16_t* op = o + row_base * kHeadDim;
+#pragma unroll
+  for (int d = 0; d < 4; ++d)
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      const int dim = 32 * d + 8 * gq + 4 * hf;
+      *(uint2*)(op + dim) =
+          make_uint2(pack_bf16x2(oacc[d][4 * gq] * inv, oacc[d][4 * gq + 1] * inv),
+                     pack_bf16x2(oacc[d][4 * gq + 2] * inv, oacc[d][4 * gq + 3] * inv));
+    }
+}
+
 template <int MODE, int SUB>
 __global__ __launch_bounds__(kThreads, 2) void attn_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
@@ -262,26 +376,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(
     const int seg = q0 / Ls;
     lst = bidx + ((size_t)(b * Hq + h) * CS + seg) * kmax;
     const int c = min(max(bcnt[(size_t)(b * Hq + h) * CS + seg], 0), kmax);
-    // Valid prefix of the list, 64 entries at a time: strictly ascending,
-    // inside [0, C_B), and not wholly after the tile's last query.
-    int nv = 0;
-    for (int base = 0; base < c; base += kWave) {
-      const int e = base + lane;
-      bool ok = false;
-      if (e < c) {
-        const int blk = lst[e];
-        const int prv = e > 0 ? lst[e - 1] : -1;
-        ok = blk > prv && blk < CB && blk * SUB * kSub <= q_last;
-      }
-      const uint64_t bad = ~__builtin_amdgcn_ballot_w64(ok);
-      if (bad != 0) {
-        nv = base + (int)__builtin_ctzll(bad);
-        break;
-      }
-      nv = base + kWave;
-    }
-    nv = min(nv, c);
-    n_steps = nv * SUB;
+    n_steps = valid_prefix<SUB>(lst, c, CB, q_last, lane) * SUB;
   } else if (MODE == kDenseCausal) {
     n_steps = q_last / kSub + 1;
   } else {
@@ -317,71 +412,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(
     __syncthreads();
     const int k0 = step_key0(i);
     const bool active = (MODE == kDenseFull) || (k0 <= qw0 + 31);
-    if (active && qw0 < N) {
-      // S^T = K Q^T for the 64 keys (two 32-key tiles).
-      f32x16 sacc[2];
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sacc[u][r] = 0.0f;
-#pragma unroll
-        for (int s = 0; s < 8; ++s)
-          sacc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(read_k(st, 32 * u + jq, s, hf), qf[s],
-                                                           sacc[u], 0, 0, 0);
-      }
-      // mask keys after the query (causal) or at / past N; branch-free
-      const bool need_mask = (MODE != kDenseFull && k0 + kSub - 1 > qw0) || (k0 + kSub > N);
-      if (need_mask) {
-        const int lim = (MODE == kDenseFull ? N - 1 : min(qrow, N - 1)) - k0 - 4 * hf;
-#pragma unroll
-        for (int u = 0; u < 2; ++u)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int kk = 32 * u + 8 * (r >> 2) + (r & 3);
-            sacc[u][r] = (kk <= lim) ? sacc[u][r] : -INFINITY;
-          }
-      }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int u = 0; u < 2; ++u)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[u][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mcand = mx * sc_log2;
-      if (__builtin_amdgcn_ballot_w64(mcand > m_i + kRescaleThreshold) != 0) {
-        const float m_new = fmaxf(m_i, mcand);
-        const float alpha = (m_new == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f(m_i - m_new);
-        l_i *= alpha;
-#pragma unroll
-        for (int d = 0; d < 4; ++d)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) oacc[d][r] *= alpha;
-        m_i = m_new;
-      }
-      const float mneg = (m_i == -INFINITY) ? 0.0f : -m_i;
-      uint4 pw[4];   // P^T as bf16, one 16-key MFMA step each
-      float lsum = 0.0f;
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        const int u = s >> 1, base = 8 * (s & 1);
-        float p[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          p[e] = __builtin_amdgcn_exp2f(fmaf(sacc[u][base + e], sc_log2, mneg));
-          lsum += p[e];
-        }
-        pw[s] = make_uint4(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
-                           pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7]));
-      }
-      l_i += lsum;
-      // O^T += V^T P^T
-#pragma unroll
-      for (int d = 0; d < 4; ++d)
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
-          oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(read_vt(st, d, s, lane),
-                                                           as_bf16x8(pw[s]), oacc[d], 0, 0, 0);
-    }
+    if (active && qw0 < N)
+      compute_step<MODE>(st, k0, qw0, qrow, N, jq, hf, lane, qf, sc_log2, oacc, m_i, l_i);
     if (i + 2 < n_steps) {
       __syncthreads();   // every wave is done reading this stage
       issue_stage(st, kh, vh, step_key0(i + 2), N, wave, lane, koff, voff);
@@ -398,18 +430,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(
   }
 
   if (qrow >= N) return;
-  const float l = l_i + __shfl_xor(l_i, 32);
-  const float inv = l > 0.0f ? 1.0f / l : 0.0f;
-  uint16_t* op = o + ((size_t)(b * Hq + h) * N + qrow) * kHeadDim;
-#pragma unroll
-  for (int d = 0; d < 4; ++d)
-#pragma unroll
-    for (int gq = 0; gq < 4; ++gq) {
-      const int dim = 32 * d + 8 * gq + 4 * hf;
-      *(uint2*)(op + dim) =
-          make_uint2(pack_bf16x2(oacc[d][4 * gq] * inv, oacc[d][4 * gq + 1] * inv),
-                     pack_bf16x2(oacc[d][4 * gq + 2] * inv, oacc[d][4 * gq + 3] * inv));
-    }
+  store_rows(o, (size_t)(b * Hq + h) * N + qrow, hf, oacc, l_i);
 }
 
 template <int MODE, int SUB>
@@ -425,7 +446,217 @@ hipError_t launch_t(const uint16_t* q, const uint16_t* k, const uint16_t* v, con
   return hipGetLastError();
 }
 
+
+// ---------------------------------------------------------------------------
+// GQA-union tiles.  One workgroup of 8 waves takes the same 128-row query tile
+// of two query heads that share a KV head (waves 0-3 the first, 4-7 the
+// second).  The heads' block lists are merged into their union (a bitmap over
+// the key blocks, compacted in ascending order); each union block is copied
+// into LDS once, and the waves of a head that did not select it skip its
+// compute while still taking part in the barriers.  Every head visits its own
+// blocks in ascending order with compute_step, so the output equals
+// attn_kernel's bit for bit.
+constexpr int kUnionThreads = 2 * kThreads;
+constexpr int kUnionWords = kUnionMaxBlocks / 32;
+
+// Stage copy by 8 waves: wave w moves rows 8 w .. 8 w + 7 of K and of V.
+__device__ __forceinline__ void issue_stage8(unsigned char* stage, const uint16_t* __restrict__ kh,
+                                             const uint16_t* __restrict__ vh, int k0, int N,
+                                             int wave, int lane, const uint32_t* koff,
+                                             const uint32_t* voff) {
+  const int pos = lane & 15;
+  const uint32_t base = (uint32_t)(uintptr_t)stage;
+  if (k0 + kSub <= N) {
+    const unsigned char* kb = (const unsigned char*)kh + (size_t)k0 * kRowBytes;
+    const unsigned char* vb = (const unsigned char*)vh + (size_t)k0 * kRowBytes;
+    const uint32_t dst0 =
+        base + (uint32_t)(8 * __builtin_amdgcn_readfirstlane(wave) * kRowBytes);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      copy16_to_lds_s(kb, koff[j], dst0 + 4 * j * kRowBytes);
+      copy16_to_lds_s(vb, voff[j], dst0 + 4 * j * kRowBytes + kTileBytes);
+    }
+    return;
+  }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int row = 8 * wave + 4 * j + (lane >> 4);
+    const int grow = min(k0 + row, N - 1);
+    const size_t roff = (size_t)grow * kHeadDim;
+    const uint32_t dst = base + (uint32_t)((8 * wave + 4 * j) * kRowBytes);
+    copy16_to_lds(kh + roff + 8 * swz(row, pos), __builtin_amdgcn_readfirstlane(dst));
+    copy16_to_lds(vh + roff + 8 * swz_v(row, pos),
+                  __builtin_amdgcn_readfirstlane(dst + kTileBytes));
+  }
+}
+
+template <int SUB>
+__global__ __launch_bounds__(kUnionThreads, 1) void attn_union_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+    const uint16_t* __restrict__ v, uint16_t* __restrict__ o, int B, int Hq, int Hkv, int N,
+    int n_tiles, int Ls, int CS, int CB, float sc_log2, const int32_t* __restrict__ bidx,
+    const int32_t* __restrict__ bcnt, int kmax) {
+  __shared__ __attribute__((aligned(1024))) unsigned char stage0[kStageBytes];
+  __shared__ __attribute__((aligned(1024))) unsigned char stage1[kStageBytes];
+  __shared__ uint32_t sel_bits[2][kUnionWords];     // the two heads' selected blocks
+  __shared__ uint32_t word_off[kUnionWords + 1];    // union entries before each word
+  __shared__ uint32_t ulist[2 * kUnionMaxList];     // block | head-0 bit 30 | head-1 bit 31
+
+  // Tile-major, heavier tiles first, the (batch, KV head, pair) index rotated
+  // by one per tile.
+  const int G = Hq / Hkv, npair = (G + 1) / 2;
+  const unsigned R = (unsigned)B * (unsigned)Hkv * (unsigned)npair;
+  if (blockIdx.x >= R * (unsigned)n_tiles) return;
+  const unsigned tr = blockIdx.x / R;
+  const unsigned rr = (blockIdx.x % R + tr) % R;
+  const int tile = n_tiles - 1 - (int)tr;
+  const int pair = (int)(rr % (unsigned)npair);
+  const int bg = (int)(rr / (unsigned)npair);
+  const int b = bg / Hkv, g = bg % Hkv;
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int side = wave >> 2, wq = wave & 3;
+  const int jq = lane & 31, hf = lane >> 5;
+  const bool has_head = 2 * pair + side < G;        // the second side of an odd G is empty
+  const int h = g * G + min(2 * pair + side, G - 1);
+  const int q0 = tile * kTileQ;
+  const int q_last = min(q0 + kTileQ - 1, N - 1);
+  const int qw0 = q0 + wq * 32;
+  const int qrow = qw0 + jq;
+
+  const uint16_t* kh = k + (size_t)(b * Hkv + g) * N * kHeadDim;
+  const uint16_t* vh = v + (size_t)(b * Hkv + g) * N * kHeadDim;
+
+  bf16x8 qf[8];
+  {
+    const uint16_t* qp = q + ((size_t)(b * Hq + h) * N + qrow) * kHeadDim + 8 * hf;
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+      qf[s] = as_bf16x8(qrow < N ? *(const uint4*)(qp + 16 * s) : make_uint4(0, 0, 0, 0));
+  }
+
+  // The union of the two heads' valid list prefixes, ascending.
+  const int seg = q0 / Ls;
+  for (int i = tid; i < 2 * kUnionWords; i += kUnionThreads) (&sel_bits[0][0])[i] = 0u;
+  __syncthreads();
+  for (int sd = 0; sd < 2; ++sd) {
+    if (2 * pair + sd >= G) continue;
+    const int hs = g * G + 2 * pair + sd;
+    const int32_t* lst = bidx + ((size_t)(b * Hq + hs) * CS + seg) * kmax;
+    const int c = min(max(bcnt[(size_t)(b * Hq + hs) * CS + seg], 0), kmax);
+    const int nv = valid_prefix<SUB>(lst, c, CB, q_last, lane);
+    for (int e = tid; e < nv; e += kUnionThreads) {
+      const int blk = lst[e];
+      atomicOr(&sel_bits[sd][blk >> 5], 1u << (blk & 31));
+    }
+  }
+  __syncthreads();
+  const int nw = (CB + 31) / 32;
+  if (wave == 0) {
+    uint32_t cnt[4], S = 0;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int wd = 4 * lane + t;
+      cnt[t] = wd < nw ? (uint32_t)__popc(sel_bits[0][wd] | sel_bits[1][wd]) : 0u;
+      S += cnt[t];
+    }
+    const uint32_t pre = wave_incl_scan_u32(S);
+    uint32_t off = pre - S;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      word_off[4 * lane + t] = off;
+      off += cnt[t];
+    }
+    if (lane == kWave - 1) word_off[kUnionWords] = pre;
+  }
+  __syncthreads();
+  for (int wd = tid; wd < nw; wd += kUnionThreads) {
+    const uint32_t a = sel_bits[0][wd], c2 = sel_bits[1][wd];
+    uint32_t u = a | c2, p = word_off[wd];
+    while (u != 0u) {
+      const int bit = __builtin_ctz(u);
+      u &= u - 1u;
+      ulist[p++] = (uint32_t)(32 * wd + bit) | (((a >> bit) & 1u) << 30) |
+                   (((c2 >> bit) & 1u) << 31);
+    }
+  }
+  __syncthreads();
+  const int n_steps = (int)word_off[kUnionWords] * SUB;
+  auto entry = [&](int i) -> uint32_t { return ulist[SUB == 1 ? i : i >> 1]; };
+  auto key0 = [&](uint32_t e, int i) -> int {
+    const int blk = (int)(e & 0x3fffffffu);
+    return (SUB == 1 ? blk : blk * SUB + (i & 1)) * kSub;
+  };
+
+  uint32_t koff[2], voff[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int row = 8 * wave + 4 * j + (lane >> 4);
+    koff[j] = (uint32_t)(row * kRowBytes + 16 * swz(row, lane & 15));
+    voff[j] = (uint32_t)(row * kRowBytes + 16 * swz_v(row, lane & 15));
+  }
+
+  f32x16 oacc[4];
+#pragma unroll
+  for (int d = 0; d < 4; ++d)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[d][r] = 0.0f;
+  float m_i = -INFINITY, l_i = 0.0f;
+
+  // The ring of attn_kernel with four copies per wave and stage.
+  auto step = [&](const int i, unsigned char* st) {
+    if (i + 1 < n_steps) EI_WAIT_VMCNT(4); else EI_WAIT_VMCNT(0);
+    __syncthreads();
+    const uint32_t e = entry(i);
+    const int k0 = key0(e, i);
+    const bool mine = has_head && ((e >> (30 + side)) & 1u) != 0u;
+    if (mine && k0 <= qw0 + 31 && qw0 < N)
+      compute_step<kSparse>(st, k0, qw0, qrow, N, jq, hf, lane, qf, sc_log2, oacc, m_i, l_i);
+    if (i + 2 < n_steps) {
+      __syncthreads();   // every wave is done reading this stage
+      issue_stage8(st, kh, vh, key0(entry(i + 2), i + 2), N, wave, lane, koff, voff);
+    }
+  };
+  EI_WAIT_VMCNT(0);
+  if (n_steps > 0) issue_stage8(stage0, kh, vh, key0(entry(0), 0), N, wave, lane, koff, voff);
+  if (n_steps > 1) issue_stage8(stage1, kh, vh, key0(entry(1), 1), N, wave, lane, koff, voff);
+  for (int i = 0; i < n_steps; i += 2) {
+    step(i, stage0);
+    if (i + 1 < n_steps) step(i + 1, stage1);
+  }
+
+  if (!has_head || qrow >= N) return;
+  store_rows(o, (size_t)(b * Hq + h) * N + qrow, hf, oacc, l_i);
+}
+
+template <int SUB>
+hipError_t launch_union_t(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                          const AttnShape& s, const int32_t* bidx, const int32_t* bcnt,
+                          uint16_t* o, hipStream_t stream) {
+  const int n_tiles = (s.N + kTileQ - 1) / kTileQ;
+  const int npair = (s.Hq / s.Hkv + 1) / 2;
+  const int64_t grid = (int64_t)s.B * s.Hkv * npair * n_tiles;
+  const float sc_log2 = (float)((double)s.softmax_scale * 1.4426950408889634);
+  hipLaunchKernelGGL((attn_union_kernel<SUB>), dim3((unsigned)grid), dim3(kUnionThreads), 0,
+                     stream, q, k, v, o, s.B, s.Hq, s.Hkv, s.N, n_tiles, s.Ls, s.CS, s.CB,
+                     sc_log2, bidx, bcnt, s.kmax);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+bool attention_union_supported(const AttnShape& s) {
+  return s.kmax <= kUnionMaxList && s.CB <= kUnionMaxBlocks;
+}
+
+hipError_t launch_attention_union(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                                  const AttnShape& s, const int32_t* block_idx,
+                                  const int32_t* block_cnt, uint16_t* o, hipStream_t stream) {
+  if (!attention_union_supported(s)) return hipErrorInvalidValue;
+  return s.Lb == 2 * kSub ? launch_union_t<2>(q, k, v, s, block_idx, block_cnt, o, stream)
+                          : launch_union_t<1>(q, k, v, s, block_idx, block_cnt, o, stream);
+}
 
 hipError_t launch_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                             const AttnShape& s, AttnMode mode, const int32_t* block_idx,

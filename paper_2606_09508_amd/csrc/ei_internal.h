@@ -65,6 +65,45 @@ __device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
 
 __device__ __forceinline__ int popc64(uint64_t m) { return __popcll(m); }
 
+// Wave-wide primitives without LDS round trips: DPP within rows of 16 lanes,
+// v_readlane across rows.
+#define EI_DPP_U32(v, ctrl, rmask, bctrl) \
+  ((uint32_t)__builtin_amdgcn_update_dpp(0, (int)(v), (ctrl), (rmask), 0xF, (bctrl)))
+__device__ __forceinline__ uint32_t rl_u32(uint32_t v, int l) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, l);
+}
+__device__ __forceinline__ uint32_t wave_max_u32_f(uint32_t v) {
+  uint32_t t;
+  t = EI_DPP_U32(v, 0xB1, 0xF, false); v = t > v ? t : v;    // quad_perm [1,0,3,2]
+  t = EI_DPP_U32(v, 0x4E, 0xF, false); v = t > v ? t : v;    // quad_perm [2,3,0,1]
+  t = EI_DPP_U32(v, 0x141, 0xF, false); v = t > v ? t : v;   // row_half_mirror
+  t = EI_DPP_U32(v, 0x140, 0xF, false); v = t > v ? t : v;   // row_mirror
+  const uint32_t a = rl_u32(v, 0), b = rl_u32(v, 16), c = rl_u32(v, 32), d = rl_u32(v, 48);
+  const uint32_t ab = a > b ? a : b, cd = c > d ? c : d;
+  return ab > cd ? ab : cd;
+}
+__device__ __forceinline__ uint32_t wave_min_u32_f(uint32_t v) {
+  uint32_t t;
+  t = EI_DPP_U32(v, 0xB1, 0xF, false); v = t < v ? t : v;
+  t = EI_DPP_U32(v, 0x4E, 0xF, false); v = t < v ? t : v;
+  t = EI_DPP_U32(v, 0x141, 0xF, false); v = t < v ? t : v;
+  t = EI_DPP_U32(v, 0x140, 0xF, false); v = t < v ? t : v;
+  const uint32_t a = rl_u32(v, 0), b = rl_u32(v, 16), c = rl_u32(v, 32), d = rl_u32(v, 48);
+  const uint32_t ab = a < b ? a : b, cd = c < d ? c : d;
+  return ab < cd ? ab : cd;
+}
+// Inclusive prefix sum over the 64 lanes (lanes without a source add 0).
+__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t x) {
+  x += EI_DPP_U32(x, 0x111, 0xF, true);   // row_shr:1
+  x += EI_DPP_U32(x, 0x112, 0xF, true);   // row_shr:2
+  x += EI_DPP_U32(x, 0x114, 0xF, true);   // row_shr:4
+  x += EI_DPP_U32(x, 0x118, 0xF, true);   // row_shr:8
+  x += EI_DPP_U32(x, 0x142, 0xA, true);   // row_bcast:15 into rows 1, 3
+  x += EI_DPP_U32(x, 0x143, 0xC, true);   // row_bcast:31 into rows 2, 3
+  return x;
+}
+
+
 // ----------------------------------------------------------------------------
 // Host launchers (arguments already validated; B, N > 0)
 // ----------------------------------------------------------------------------
@@ -106,6 +145,15 @@ struct AttnShape {
 };
 
 enum AttnMode { kSparse = 0, kDenseCausal = 1, kDenseFull = 2 };
+
+// GQA-union tiles (two query heads of a KV group per workgroup): limits of
+// the merged list held in LDS.
+constexpr int kUnionMaxList = 128;     // kmax
+constexpr int kUnionMaxBlocks = 8192;  // C_B
+bool attention_union_supported(const AttnShape& s);
+hipError_t launch_attention_union(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                                  const AttnShape& s, const int32_t* block_idx,
+                                  const int32_t* block_cnt, uint16_t* o, hipStream_t stream);
 
 hipError_t launch_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                             const AttnShape& s, AttnMode mode, const int32_t* block_idx,

@@ -250,3 +250,19 @@ def test_sizes_whose_grids_overflow_are_refused(L):
                                     None) == -2
     ok = eb.Dims(1, 1 << 17, 1 << 10, 1 << 20, 128)       # 2^17 x 2^13 = 2^30 workgroups
     assert L.ei_num_segments(ok, t) == (1 << 20) // 128
+
+
+def test_gqa_union_attention_limits(L):
+    """The GQA-union mode holds the merged list in LDS: kmax <= 128 and
+    C_B <= 8192, else EI_ERR_UNSUPPORTED; otherwise it validates like
+    ei_sparse_prefill_attn."""
+    d, t = eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(128, 64)
+    call = L.ei_sparse_prefill_attn_gqa_union
+    assert call(FAKE, FAKE, FAKE, d, t, 0.088, FAKE, FAKE, 129, FAKE, None) == -3
+    long = eb.Dims(1, 4, 1, 8192 * 64 + 64, 128)
+    assert call(FAKE, FAKE, FAKE, long, t, 0.088, FAKE, FAKE, 98, FAKE, None) == -3
+    assert call(FAKE, FAKE, FAKE, d, t, 0.088, FAKE, FAKE, 0, FAKE, None) == -2
+    assert call(FAKE, FAKE, None, d, t, 0.088, FAKE, FAKE, 98, FAKE, None) == -1
+    assert call(FAKE, FAKE, _off(FAKE, 8), d, t, 0.088, FAKE, FAKE, 98, FAKE, None) == -3
+    assert call(FAKE, FAKE, FAKE, eb.Dims(0, 4, 1, 1024, 128), t, 0.088, None, None, 98, None,
+                None) == 0

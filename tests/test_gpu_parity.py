@@ -181,6 +181,34 @@ def test_deterministic():
     assert torch.equal(a["o"], b["o"])
 
 
+@pytest.mark.parametrize("wl,seed,case", [
+    ("c1", 5, dict()),                                    # G = 4: two pairs
+    ("c1", 5, dict(N=1000)),                              # ragged tail
+    ("c1", 6, dict(Hq=7, Hkv=1, N=512)),                  # odd G: the last pair has one head
+    ("c1", 6, dict(Hq=4, Hkv=4)),                         # G = 1: one head per workgroup
+    ("c1", 7, dict(Ls=256, Lb=128, N=1280, base_budget=512)),   # two sub-blocks per block
+    ("c1", 7, dict(B=2, Hq=8, Hkv=2, N=640)),
+    ("c1", 8, dict(N=2048, base_budget=64)),              # short lists, large unions
+    ("c1", 8, dict(N=65)),
+    ("c2", 2, dict(N=16384)),
+    ("c4", 1, dict(N=8192)),                              # G = 7 with real lists
+], ids=lambda x: x if isinstance(x, str) else None)
+def test_gqa_union_attention_equals_per_head(wl, seed, case):
+    """GQA-union tiles (two heads of a KV group share each union block's copy)
+    give bitwise the per-head kernel's output."""
+    w = synth.make(wl, seed, **case)
+    say(f"[union] {wl} seed={seed} {case}")
+    q, k, v = to_dev(w.q), to_dev(w.k), to_dev(w.v)
+    ls, en = eb.entropy_probe(q, k, w.Ls, w.Lb, w.probe_scale)
+    sel = eb.select_blocks(ls, en, w.N, w.Ls, w.Lb, w.e_t, w.alpha, w.delta_t, w.base_budget,
+                           w.mult, n_kv_heads=w.Hkv)
+    o = eb.sparse_prefill_attn(q, k, v, sel["idx"], sel["cnt"], w.Ls, w.Lb, w.softmax_scale)
+    ou = eb.sparse_prefill_attn(q, k, v, sel["idx"], sel["cnt"], w.Ls, w.Lb, w.softmax_scale,
+                                gqa_union=True)
+    torch.cuda.synchronize()
+    assert torch.equal(ou, o)
+
+
 def test_binding_refuses_mismatched_tensors():
     """k / v / score tensors that do not match q's sizes raise before any launch."""
     w = synth.make("c1", 4, N=512)
