@@ -268,6 +268,25 @@ def main():
     torch.cuda.synchronize()
     dense_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in de]))
 
+    # GQA-union tiles on the same lists: time and bitwise agreement with the
+    # per-head kernel (the union mode is a measured alternative, not the path)
+    union = None
+    if w.kmax <= 128:
+        ou = torch.empty_like(q)
+        eb.sparse_prefill_attn(q, k, v, bufs["sel"]["idx"], bufs["sel"]["cnt"], w.Ls, w.Lb,
+                               w.softmax_scale, ou, gqa_union=True)
+        torch.cuda.synchronize()
+        ue = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(5)]
+        for e in ue:
+            e[0].record()
+            eb.sparse_prefill_attn(q, k, v, bufs["sel"]["idx"], bufs["sel"]["cnt"], w.Ls, w.Lb,
+                                   w.softmax_scale, ou, gqa_union=True)
+            e[1].record()
+        torch.cuda.synchronize()
+        union = {"ms": round(float(np.median([e[0].elapsed_time(e[1]) for e in ue])), 4),
+                 "bitwise_equal_to_per_head": bool(torch.equal(ou, bufs["out"]))}
+        del ou
+
     cnt = bufs["sel"]["cnt"].cpu().numpy()
     idx = bufs["sel"]["idx"].cpu().numpy()
     rigid = bufs["sel"]["rigid"].cpu().numpy()
@@ -332,6 +351,7 @@ def main():
         "sparse_attn_tflops": round(sparse_tflops, 2),
         "sparse_attn_tile_tflops": round(sparse_tile_tflops, 2),
         "mfma_busy_counter": read_counter_file(SQ_FILE, "mfma_busy_fraction"),
+        "sparse_attn_gqa_union": union,
         "dense_ms": round(dense_ms, 3),
         "dense_tflops": round(dense_tflops, 2),
         "speedup_vs_dense": round(dense_ms / pipe_ms, 3),
