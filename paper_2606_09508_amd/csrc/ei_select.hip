@@ -229,8 +229,11 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
       // is the first at which the keys above ls's buckets plus the running
       // count reach kk (lane ls itself reaches it, so the ballot is not 0)
       const uint32_t acc0 = rl_u32(suf - S, ls);
-      const int bin = 32 * ls + 31 - (lane & 31);
-      const uint32_t bt = lane < 32 ? (hist[bin >> 1] >> (16 * (bin & 1))) & 0xffffu : 0u;
+      uint32_t bt = 0u;
+      if (lane < 32) {
+        const int bin = 32 * ls + 31 - lane;
+        bt = (hist[bin >> 1] >> (16 * (bin & 1))) & 0xffffu;
+      }
       const uint32_t run = wave_incl_scan_u32(bt);
       const uint64_t hit = __ballot(lane < 32 && acc0 + run >= (uint32_t)kk);
       const int tb = (int)__builtin_ctzll(hit);
