@@ -4,7 +4,7 @@
 //  budget_kernel  one workgroup per (b, query head): the rigid test over all
 //                 segment entropies, the ratios |e_s - e_{s-1}| / e_{s-1} in
 //                 parallel, the clamped budget recurrence (inherently
-//                 sequential; one wave, increments read across lanes) and
+//                 sequential; one wave, increments broadcast from LDS) and
 //                 k_s = min(floor(B_s / L_B), s r).
 //                 Variants: the entropies may be the GQA group's means
 //                 (binary64 sum in head order / G, rounded to binary32), and
@@ -74,7 +74,13 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(
   double Bprev = B0;   // meaningful in wave 0 only
   for (int c0 = 0; c0 < CS; c0 += kChunk) {
     const int n = min(kChunk, CS - c0);
-    for (int i = tid; i < n; i += kThreads) {
+    // the increments are padded with zeros to a whole number of waves
+    const int npad = (n + kWave - 1) / kWave * kWave;
+    for (int i = tid; i < npad; i += kThreads) {
+      if (i >= n) {
+        delta[i] = 0.0;
+        continue;
+      }
       const int s = c0 + i;
       const float es = E(s);
       // B_0 = B_h, and a rigid segment of the per-segment rule takes B_h:
@@ -91,23 +97,18 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(
     }
     __syncthreads();
     if (tid < kWave) {
-      // Wave 0 runs the recurrence 64 segments at a time: lane j holds the
-      // increment of segment i0 + j and each step reads it with v_readlane,
-      // so the dependent chain is the add and the two clamps.  The clamps
-      // as fmax / fmin give the same value as the comparisons in every case
-      // (NaN and -inf -> B_0, +inf -> 3 B_0).  Every lane carries the same
-      // B_prev and writes the same value; past the chunk's end the steps run
-      // on zero increments and their results are not read.
+      // Wave 0 runs the recurrence 64 segments at a time, every lane reading
+      // each increment from LDS as a broadcast (the loads of a group are
+      // independent of the chain and issue ahead of it), so the dependent
+      // chain is the add and the two clamps.  The clamps as fmax / fmin give
+      // the same value as the comparisons in every case (NaN and -inf -> B_0,
+      // +inf -> 3 B_0).  Every lane carries the same B_prev and writes the
+      // same value; past the chunk's end the steps run on the zero padding
+      // and their results are not read.
       for (int i0 = 0; i0 < n; i0 += kWave) {
-        const double dl = tid < n - i0 ? delta[i0 + tid] : 0.0;
-        const uint64_t dbits = __builtin_bit_cast(uint64_t, dl);
-        const int dlo = (int)(uint32_t)dbits, dhi = (int)(uint32_t)(dbits >> 32);
 #pragma unroll
         for (int j = 0; j < kWave; ++j) {
-          const uint64_t bits =
-              ((uint64_t)(uint32_t)__builtin_amdgcn_readlane(dhi, j) << 32) |
-              (uint64_t)(uint32_t)__builtin_amdgcn_readlane(dlo, j);
-          Bprev = fmin(fmax(Bprev + __builtin_bit_cast(double, bits), B0), cap);
+          Bprev = fmin(fmax(Bprev + delta[i0 + j], B0), cap);
           Bs[i0 + j] = Bprev;
         }
       }
