@@ -176,11 +176,17 @@ __device__ __forceinline__ bf16x8 read_vt(const unsigned char* stage, int dt, in
 #define EI_WAIT_VMCNT(n) \
   __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (7 << 4) | (15 << 8))
 
-// Lazy rescaling: the running maximum is only raised when a new score exceeds
-// it by more than 2^8 (base-2 units), so exp2 arguments stay <= 8 and O, l are
-// rescaled rarely; O and l always share the same reference, so the result is
-// the exact softmax.
+// Lazy rescaling: the running maximum m is only raised when a new score
+// exceeds it by more than 8 (base-2 units), so O and l are rescaled rarely; O
+// and l always share the same reference, so the result is the exact softmax.
+// A sub-block's probabilities are first formed against the current m without
+// its row maximum: if every lane's sum of them stays <= 2^32 (so each
+// probability does, and O, l stay far from overflow), they are kept.
+// Otherwise (the first sub-block, a score more than 32 above m, or an
+// overflow) the wave takes the row maxima, raises m by the rule above and
+// forms them again.
 constexpr float kRescaleThreshold = 8.0f;
+constexpr float kFastLimit = 0x1p32f;
 
 // Valid prefix of a block list of c entries, 64 at a time: strictly
 // ascending, inside [0, C_B), and not wholly after the tile's last query.
@@ -237,37 +243,47 @@ __device__ __forceinline__ void compute_step(const unsigned char* st, int k0, in
         sacc[u][r] = (kk <= lim) ? sacc[u][r] : -INFINITY;
       }
   }
-  float mx = -INFINITY;
-#pragma unroll
-  for (int u = 0; u < 2; ++u)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[u][r]);
-  mx = fmaxf(mx, __shfl_xor(mx, 32));
-  const float mcand = mx * sc_log2;
-  if (__builtin_amdgcn_ballot_w64(mcand > m_i + kRescaleThreshold) != 0) {
-    const float m_new = fmaxf(m_i, mcand);
-    const float alpha = (m_new == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f(m_i - m_new);
-    l_i *= alpha;
-#pragma unroll
-    for (int d = 0; d < 4; ++d)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[d][r] *= alpha;
-    m_i = m_new;
-  }
-  const float mneg = (m_i == -INFINITY) ? 0.0f : -m_i;
   uint4 pw[4];   // P^T as bf16, one 16-key MFMA step each
-  float lsum = 0.0f;
+  float lsum;
+  auto probs = [&](float mneg) {
+    lsum = 0.0f;
 #pragma unroll
-  for (int s = 0; s < 4; ++s) {
-    const int u = s >> 1, base = 8 * (s & 1);
-    float p[8];
+    for (int s = 0; s < 4; ++s) {
+      const int u = s >> 1, base = 8 * (s & 1);
+      float p[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      p[e] = __builtin_amdgcn_exp2f(fmaf(sacc[u][base + e], sc_log2, mneg));
-      lsum += p[e];
+      for (int e = 0; e < 8; ++e) {
+        p[e] = __builtin_amdgcn_exp2f(fmaf(sacc[u][base + e], sc_log2, mneg));
+        lsum += p[e];
+      }
+      pw[s] = make_uint4(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
+                         pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7]));
     }
-    pw[s] = make_uint4(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
-                       pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7]));
+  };
+  bool kept = false;
+  if (__builtin_amdgcn_ballot_w64(m_i == -INFINITY) == 0) {
+    probs(-m_i);
+    kept = __builtin_amdgcn_ballot_w64(!(lsum <= kFastLimit)) == 0;   // NaN fails too
+  }
+  if (!kept) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[u][r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float mcand = mx * sc_log2;
+    if (__builtin_amdgcn_ballot_w64(mcand > m_i + kRescaleThreshold) != 0) {
+      const float m_new = fmaxf(m_i, mcand);
+      const float alpha = (m_new == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f(m_i - m_new);
+      l_i *= alpha;
+#pragma unroll
+      for (int d = 0; d < 4; ++d)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[d][r] *= alpha;
+      m_i = m_new;
+    }
+    probs((m_i == -INFINITY) ? 0.0f : -m_i);
   }
   l_i += lsum;
   // O^T += V^T P^T
