@@ -171,6 +171,57 @@ def test_full_budget_sparse_is_dense_bitwise():
     assert torch.equal(od, r["o"])
 
 
+def _jump_inputs(N=1000, Hq=2, seed=5):
+    """Scores that rise part way through each row: q_0 = 4 for every query,
+    keys 320..383 carry k_0 = 80 (about 40 base-2 units over the earlier
+    blocks' maximum), keys 640..703 k_0 = 400 (2^-x of the earlier maximum
+    overflows fp32) and keys 900..909 k_0 = -400 (their probabilities
+    underflow to zero)."""
+    rng = np.random.default_rng(seed)
+    D = 128
+    qf = rng.standard_normal((1, Hq, N, D)).astype(np.float32)
+    kf = rng.standard_normal((1, 1, N, D)).astype(np.float32)
+    vf = rng.standard_normal((1, 1, N, D)).astype(np.float32)
+    qf[..., 0] = 4.0
+    kf[:, :, 320:384, 0] = 80.0
+    kf[:, :, 640:704, 0] = 400.0
+    kf[:, :, 900:910, 0] = -400.0
+    w = synth.make("c1", seed, Hq=Hq, N=N, generate_tensors=False)
+    w.q, w.k, w.v = (synth.to_bf16_bits(x) for x in (qf, kf, vf))
+    return w
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_dense_attention_running_max_jumps(causal):
+    """The running maximum is left behind by more than the probabilities'
+    2^32 limit, and by enough to overflow exp2, in the middle of rows: the
+    kernel must take the row maxima and rescale; every row against the fp64
+    oracle."""
+    w = _jump_inputs()
+    say(f"[dense jumps] causal={causal}")
+    o = eb.dense_prefill_attn(to_dev(w.q), to_dev(w.k), to_dev(w.v), w.softmax_scale, causal)
+    torch.cuda.synchronize()
+    rows = np.array([[0, h, i] for h in range(w.Hq) for i in range(w.N)], np.int32)
+    ref = oracle.attention(w.q, w.k, w.v, rows, w.softmax_scale, causal)
+    got = bf16_to_f64(o)[rows[:, 0], rows[:, 1], rows[:, 2]]
+    assert np.isfinite(got).all()
+    assert np.abs(got - ref).max() <= ATTN_ABS
+
+
+def test_sparse_attention_running_max_jumps():
+    """The same inputs through probe, selection and sparse attention: every
+    row against the oracle on the GPU's block lists."""
+    w = _jump_inputs()
+    say("[sparse jumps]")
+    r = run_path(w)
+    rows = np.array([[0, h, i] for h in range(w.Hq) for i in range(w.N)], np.int32)
+    ref = oracle.attention(w.q, w.k, w.v, rows, w.softmax_scale, True, r["sel"]["idx"],
+                           r["sel"]["cnt"], w.Ls, w.Lb)
+    got = bf16_to_f64(r["o"])[rows[:, 0], rows[:, 1], rows[:, 2]]
+    assert np.isfinite(got).all()
+    assert np.abs(got - ref).max() <= ATTN_ABS
+
+
 def test_deterministic():
     w = synth.make("c2", 3, N=4096)
     a = run_path(w)
