@@ -204,7 +204,12 @@ ei_status ei_select_blocks_mode(const float* log_scores, const float* entropy, e
  * A list is read up to block_cnt (clamped to [0, kmax]) and stops at the
  * first entry that is negative, >= C_B or not above its predecessor, so a
  * malformed list never leads to an out-of-bounds access.  A query with no
- * visible key gets a zero row.
+ * visible key gets a zero row.  The probabilities are formed against a
+ * running maximum that may trail the row's maximum by up to 32 (base 2), so
+ * each is at most 2^32 before it is accumulated: O stays finite while
+ * 2^32 * (keys attended) * max |v| is inside the fp32 range (|v| < 2^79 at
+ * 2^17 keys); larger scores, and an overflow of that bound's exponentials,
+ * make the kernel rescale first.
  *
  * Errors: EI_ERR_NULL, EI_ERR_SHAPE, EI_ERR_UNSUPPORTED, EI_ERR_LAUNCH.
  */
