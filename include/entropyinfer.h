@@ -208,8 +208,8 @@ ei_status ei_select_blocks_mode(const float* log_scores, const float* entropy, e
  * running maximum that may trail the row's maximum by up to 32 (base 2), so
  * each is at most 2^32 before it is accumulated: O stays finite while
  * 2^32 * (keys attended) * max |v| is inside the fp32 range (|v| < 2^79 at
- * 2^17 keys); larger scores, and an overflow of that bound's exponentials,
- * make the kernel rescale first.
+ * 2^17 keys).  A sub-block in which a lane's probabilities sum past 2^32
+ * (or overflow) is formed again after the row maximum is raised.
  *
  * Errors: EI_ERR_NULL, EI_ERR_SHAPE, EI_ERR_UNSUPPORTED, EI_ERR_LAUNCH.
  */
