@@ -328,6 +328,8 @@ hipError_t launch_topk_t(const float* log_scores, const int32_t* kb, const Selec
 
 }  // namespace
 
+// the longest row (128 slots per lane) must fit the histogram's 16-bit counters
+static_assert(128 * kWave < (1 << 16), "a row's keys must fit one 16-bit bucket counter");
 bool select_supported(const SelectShape& s) { return s.CB <= 128 * kWave; }
 
 hipError_t launch_select(const float* log_scores, const float* entropy, const SelectShape& s,
