@@ -42,10 +42,15 @@ def sources_hash(paths) -> str:
     return h.hexdigest()[:16]
 
 
-def read_counter_file(path, key):
+# the workload and seed the committed counter summaries were collected on
+COUNTER_WORKLOAD = ("c3", 0)
+
+
+def read_counter_file(path, key, workload=COUNTER_WORKLOAD):
     """A value from a committed rocprofv3 counter summary of the sparse
-    attention kernel, if the summary was taken on the current kernel source."""
-    if not os.path.exists(path):
+    attention kernel, if the summary was taken on the current kernel source
+    and on this (workload, seed)."""
+    if tuple(workload) != COUNTER_WORKLOAD or not os.path.exists(path):
         return None
     kv = {}
     for line in open(path):
@@ -60,9 +65,9 @@ def read_counter_file(path, key):
         return None
 
 
-def read_traffic():
+def read_traffic(workload=COUNTER_WORKLOAD):
     """HBM bytes per launch of the sparse attention kernel."""
-    return read_counter_file(TRAFFIC_FILE, "hbm_bytes_per_launch")
+    return read_counter_file(TRAFFIC_FILE, "hbm_bytes_per_launch", workload)
 
 
 def tile_flops(cnt: np.ndarray, N: int, Ls: int, Lb: int) -> float:
@@ -308,7 +313,7 @@ def main():
                     + 4.0 * w.B * w.Hq * w.CS * (w.kmax + 2) + w.B * w.Hq)
     total_ms = probe_ms + select_ms + sparse_ms
 
-    traffic = read_traffic()
+    traffic = read_traffic((args.workload, args.seed))
     roofline = {"kernel": "attn_kernel<sparse>", "bound": "mfma",
                 "achieved": round(sparse_tflops, 2), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(sparse_tflops / PEAK_BF16_TFLOPS, 4),
@@ -350,7 +355,8 @@ def main():
         "mfma_util": round(sparse_tflops / PEAK_BF16_TFLOPS, 4),
         "sparse_attn_tflops": round(sparse_tflops, 2),
         "sparse_attn_tile_tflops": round(sparse_tile_tflops, 2),
-        "mfma_busy_counter": read_counter_file(SQ_FILE, "mfma_busy_fraction"),
+        "mfma_busy_counter": read_counter_file(SQ_FILE, "mfma_busy_fraction",
+                                                (args.workload, args.seed)),
         "sparse_attn_gqa_union": union,
         "dense_ms": round(dense_ms, 3),
         "dense_tflops": round(dense_tflops, 2),
