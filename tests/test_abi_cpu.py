@@ -266,3 +266,29 @@ def test_gqa_union_attention_limits(L):
     assert call(FAKE, FAKE, _off(FAKE, 8), d, t, 0.088, FAKE, FAKE, 98, FAKE, None) == -3
     assert call(FAKE, FAKE, FAKE, eb.Dims(0, 4, 1, 1024, 128), t, 0.088, None, None, 98, None,
                 None) == 0
+
+
+def test_bench_counter_figures_are_scoped():
+    """bench.py takes traffic / matrix-busy figures from the committed counter
+    summaries only for the workload and seed they were collected on, and only
+    while their recorded kernel-source hash is the current one."""
+    import os
+    import shutil
+    import sys
+    import tempfile
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    sys.path.insert(0, root)
+    import bench
+    for wl in (("c1", 0), ("c3", 1), ("c5", 0)):
+        assert bench.read_traffic(wl) is None
+        assert bench.read_counter_file(bench.SQ_FILE, "mfma_busy_fraction", wl) is None
+    # a summary whose hash is not the current source's is ignored
+    with tempfile.TemporaryDirectory() as d:
+        p = os.path.join(d, "t.txt")
+        shutil.copy(bench.TRAFFIC_FILE, p)
+        good = bench.read_counter_file(p, "hbm_bytes_per_launch")
+        txt = open(p).read()
+        cur = bench.sources_hash(bench.ATTN_SOURCES)
+        assert (good is not None) == (f"attn_source_hash: {cur}" in txt)
+        open(p, "w").write(txt.replace("attn_source_hash:", "attn_source_hash: 0"))
+        assert bench.read_counter_file(p, "hbm_bytes_per_launch") is None
