@@ -19,10 +19,13 @@
  *  - bf16 tensors are passed as uint16_t bit patterns.
  *  - Q is [B][Hq][N][D], K and V are [B][Hkv][N][D]; query head h reads key
  *    head h / (Hq / Hkv) (grouped-query attention).  D must be 128.
- *  - Segment size L_S and block size L_B (Section 4.1): L_B is 64 or 128,
- *    L_S is a multiple of 128 and of L_B.  C_S = ceil(N / L_S) segments,
- *    C_B = ceil(N / L_B) key blocks, r = L_S / L_B.  A ragged tail (N not a
+ *  - Segment size L_S and block size L_B (Section 4.1): L_B is 64 or 128
+ *    (another L_B: EI_ERR_UNSUPPORTED), L_S a positive multiple of 128 and of
+ *    L_B (else EI_ERR_SHAPE).  C_S = ceil(N / L_S) segments, C_B =
+ *    ceil(N / L_B) key blocks, r = L_S / L_B.  A ragged tail (N not a
  *    multiple of L_S) forms a short last segment / block.
+ *  - Scales: softmax_scale must be finite and > 0, probe_scale finite (else
+ *    EI_ERR_SHAPE).
  *  - `stream` is a hipStream_t (NULL = the default stream).  Calls are
  *    asynchronous; outputs are valid once the stream is synchronised.
  *  - Every argument is validated on the host before anything is launched; a
@@ -125,7 +128,7 @@ size_t ei_probe_workspace_bytes(ei_dims dims, ei_tiling tiling);
  * -sum_j A ln A (natural log, Section 3).
  *
  *   q, k         bf16 [B][Hq][N][D], [B][Hkv][N][D]
- *   probe_scale  multiplies the logits; 1.0 is Algorithm 2 as printed
+ *   probe_scale  multiplies the logits (finite); 1.0 is Algorithm 2 as printed
  *   log_scores   out, fp32 [B][Hq][C_S][C_B]: ln A for j < n_vis(s); entries
  *                with j >= n_vis(s) are left untouched
  *   entropy      out, fp32 [B][Hq][C_S]
@@ -196,7 +199,7 @@ ei_status ei_select_blocks_mode(const float* log_scores, const float* entropy, e
  * online softmax, bf16 output.
  *
  *   q, k, v        bf16 [B][Hq][N][D], [B][Hkv][N][D], [B][Hkv][N][D]
- *   softmax_scale  usually 1 / sqrt(D)
+ *   softmax_scale  usually 1 / sqrt(D); finite and > 0
  *   block_idx      i32 [B][Hq][C_S][kmax] strictly ascending block indices
  *   block_cnt      i32 [B][Hq][C_S]
  *   o              out, bf16 [B][Hq][N][D]
@@ -211,7 +214,8 @@ ei_status ei_select_blocks_mode(const float* log_scores, const float* entropy, e
  * 2^17 keys).  A sub-block in which a lane's probabilities sum past 2^32
  * (or overflow) is formed again after the row maximum is raised.
  *
- * Errors: EI_ERR_NULL, EI_ERR_SHAPE, EI_ERR_UNSUPPORTED, EI_ERR_LAUNCH.
+ * Errors: EI_ERR_NULL, EI_ERR_SHAPE (also kmax <= 0 or a softmax_scale that is
+ * not finite and positive), EI_ERR_UNSUPPORTED, EI_ERR_LAUNCH.
  */
 ei_status ei_sparse_prefill_attn(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                                  ei_dims dims, ei_tiling tiling, float softmax_scale,
@@ -242,7 +246,8 @@ ei_status ei_sparse_prefill_attn_gqa_union(const uint16_t* q, const uint16_t* k,
  * (keys j <= i) when `causal` is non-zero, else over all N keys; same tile
  * code and numerics as ei_sparse_prefill_attn.
  *
- * Errors: EI_ERR_NULL, EI_ERR_SHAPE, EI_ERR_UNSUPPORTED, EI_ERR_LAUNCH.
+ * Errors: EI_ERR_NULL, EI_ERR_SHAPE (also a softmax_scale that is not finite
+ * and positive), EI_ERR_UNSUPPORTED, EI_ERR_LAUNCH.
  */
 ei_status ei_dense_prefill_attn(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                                 ei_dims dims, float softmax_scale, int32_t causal,
@@ -275,9 +280,16 @@ size_t ei_prefill_workspace_bytes(ei_dims dims, ei_tiling tiling);
  *                      ordered after all the work: synchronising `stream`
  *                      makes every output valid.  Both streams must be of
  *                      default priority.
+ *   event              a hipEvent_t created by the caller (any flags;
+ *                      hipEventDisableTiming is the cheapest) on the device
+ *                      of the streams; the call records it on both streams to
+ *                      order them, so it must not be in use by concurrent
+ *                      work.  Required from N = 16384 tokens on (the
+ *                      pipelined regime); may be NULL below.
  *
  * Errors: those of the three calls, plus EI_ERR_SHAPE if stream_aux is NULL
- * or equal to stream, and EI_ERR_LAUNCH if an event cannot be created.
+ * or equal to stream, EI_ERR_NULL if the pipelined regime has no event, and
+ * EI_ERR_LAUNCH if an event record or stream wait fails.
  */
 ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                                     ei_dims dims, ei_tiling tiling, double probe_scale,
@@ -286,7 +298,7 @@ ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const 
                                     uint8_t* head_is_rigid, int32_t* budget_blocks,
                                     int32_t* block_idx, int32_t* block_cnt, uint16_t* o,
                                     void* workspace, size_t workspace_bytes, void* stream,
-                                    void* stream_aux);
+                                    void* stream_aux, void* event);
 
 #ifdef __cplusplus
 }

@@ -85,7 +85,7 @@ def lib() -> ctypes.CDLL:
         L.ei_entropy_guided_prefill.argtypes = [_VP, _VP, _VP, Dims, Tiling, ctypes.c_double,
                                                 BudgetParams, ctypes.c_int32, ctypes.c_int32,
                                                 ctypes.c_float, _VP, _VP, _VP, _VP, _VP, _VP,
-                                                _VP, _VP, ctypes.c_size_t, _VP, _VP]
+                                                _VP, _VP, ctypes.c_size_t, _VP, _VP, _VP]
         L.ei_sparse_prefill_attn_gqa_union.restype = ctypes.c_int
         L.ei_sparse_prefill_attn_gqa_union.argtypes = L.ei_sparse_prefill_attn.argtypes
         L.ei_dense_prefill_attn.restype = ctypes.c_int
@@ -305,6 +305,7 @@ def dense_prefill_attn(q, k, v, softmax_scale: float | None = None, causal: bool
 
 
 _AUX_STREAMS: dict = {}
+_EVENTS: dict = {}
 
 
 def _aux_stream(device) -> torch.cuda.Stream:
@@ -313,6 +314,18 @@ def _aux_stream(device) -> torch.cuda.Stream:
     if idx not in _AUX_STREAMS:
         _AUX_STREAMS[idx] = torch.cuda.Stream(device=idx)
     return _AUX_STREAMS[idx]
+
+
+def _order_event(device) -> torch.cuda.Event:
+    """The event the pipelined path uses to order its two streams, one per
+    device, created once (torch creates the HIP event on its first record)."""
+    idx = torch.device(device).index or 0
+    if idx not in _EVENTS:
+        ev = torch.cuda.Event()
+        with torch.cuda.device(idx):
+            ev.record(torch.cuda.current_stream(idx))
+        _EVENTS[idx] = ev
+    return _EVENTS[idx]
 
 
 def prefill_workspace_bytes(dims: Dims, seg_len: int, block_len: int) -> int:
@@ -353,13 +366,15 @@ def entropy_guided_prefill(q, k, v, seg_len: int = 128, block_len: int = 64,
         bufs["workspace"] = ws = torch.empty((need,), dtype=torch.uint8, device=dev)
     scale = (1.0 / math.sqrt(D)) if softmax_scale is None else float(softmax_scale)
     aux = _aux_stream(dev)
+    ev = _order_event(dev)
     with torch.cuda.device(dev):
         st = lib().ei_entropy_guided_prefill(
             _ptr(q), _ptr(k), _ptr(v), d, Tiling(seg_len, block_len), float(probe_scale),
             budget_params(e_t, alpha, delta_t, base_budget, mult), int(mode), km, scale,
             _ptr(bufs["log_scores"]), _ptr(bufs["entropy"]), _ptr(bufs["rigid"]),
             _ptr(bufs["budget"]), _ptr(bufs["idx"]), _ptr(bufs["cnt"]), _ptr(bufs["out"]),
-            _ptr(ws), ws.numel(), _stream(q), ctypes.c_void_p(aux.cuda_stream))
+            _ptr(ws), ws.numel(), _stream(q), ctypes.c_void_p(aux.cuda_stream),
+            ctypes.c_void_p(ev.cuda_event))
     _check("ei_entropy_guided_prefill", st)
     # keep the buffers alive until the auxiliary stream's work has used them
     for t in list(bufs.values()) + [q, k, v]:

@@ -10,7 +10,7 @@
 
 namespace {
 
-constexpr int32_t kAbiVersion = 3;
+constexpr int32_t kAbiVersion = 4;
 
 // ei_entropy_guided_prefill pipelines over KV-head groups from this length on.
 constexpr int64_t kPipelineMinTokens = 16384;
@@ -35,9 +35,17 @@ ei_status check_dims(const ei_dims& d) {
 
 ei_status check_tiling(const ei_tiling& t) {
   if (t.block_len != 64 && t.block_len != 128) return EI_ERR_UNSUPPORTED;
-  if (t.seg_len <= 0 || t.seg_len % 128 || t.seg_len % t.block_len) return EI_ERR_UNSUPPORTED;
+  if (t.seg_len <= 0 || t.seg_len % 128 || t.seg_len % t.block_len) return EI_ERR_SHAPE;
   return EI_OK;
 }
+
+// The attention kernels mask scores to -inf before scaling and take the row
+// maximum of the raw scores, which is the maximum of the scaled ones only for
+// a positive scale: softmax_scale must be finite and > 0.
+bool scale_ok(float s) { return s > 0.0f && s <= 3.402823466e38f; }
+// probe_scale multiplies binary64 logits; any finite value (0 and negative
+// values included) is meaningful.
+bool probe_scale_ok(double s) { return s == s && s - s == 0.0; }
 
 Sizes sizes(const ei_dims& d, const ei_tiling* t) {
   Sizes s{d.batch, d.n_q_heads, d.n_kv_heads, d.seq_len, d.head_dim, 0, 0, 0};
@@ -124,7 +132,7 @@ ei_status ei_entropy_probe(const uint16_t* q, const uint16_t* k, ei_dims dims, e
   ei_status st = check_dims(dims);
   if (st != EI_OK) return st;
   if ((st = check_tiling(tiling)) != EI_OK) return st;
-  if (!(probe_scale == probe_scale)) return EI_ERR_SHAPE;
+  if (!probe_scale_ok(probe_scale)) return EI_ERR_SHAPE;
   const Sizes z = sizes(dims, &tiling);
   if (z.B == 0 || z.N == 0) return EI_OK;
   if (!q || !k || !log_scores || !entropy) return EI_ERR_NULL;
@@ -179,7 +187,7 @@ ei_status ei_sparse_prefill_attn(const uint16_t* q, const uint16_t* k, const uin
   ei_status st = check_dims(dims);
   if (st != EI_OK) return st;
   if ((st = check_tiling(tiling)) != EI_OK) return st;
-  if (kmax <= 0 || !(softmax_scale == softmax_scale)) return EI_ERR_SHAPE;
+  if (kmax <= 0 || !scale_ok(softmax_scale)) return EI_ERR_SHAPE;
   const Sizes z = sizes(dims, &tiling);
   if (z.B == 0 || z.N == 0) return EI_OK;
   if (!q || !k || !v || !block_idx || !block_cnt || !o) return EI_ERR_NULL;
@@ -198,7 +206,7 @@ ei_status ei_sparse_prefill_attn_gqa_union(const uint16_t* q, const uint16_t* k,
   ei_status st = check_dims(dims);
   if (st != EI_OK) return st;
   if ((st = check_tiling(tiling)) != EI_OK) return st;
-  if (kmax <= 0 || !(softmax_scale == softmax_scale)) return EI_ERR_SHAPE;
+  if (kmax <= 0 || !scale_ok(softmax_scale)) return EI_ERR_SHAPE;
   const Sizes z = sizes(dims, &tiling);
   if (z.B == 0 || z.N == 0) return EI_OK;
   if (!q || !k || !v || !block_idx || !block_cnt || !o) return EI_ERR_NULL;
@@ -228,14 +236,14 @@ ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const 
                                     uint8_t* head_is_rigid, int32_t* budget_blocks,
                                     int32_t* block_idx, int32_t* block_cnt, uint16_t* o,
                                     void* workspace, size_t workspace_bytes, void* stream,
-                                    void* stream_aux) {
+                                    void* stream_aux, void* event) {
   // validate the whole problem as the three calls would
   ei_status st = check_dims(dims);
   if (st != EI_OK) return st;
   if ((st = check_tiling(tiling)) != EI_OK) return st;
   if ((st = check_params(params)) != EI_OK) return st;
   if (mode < EI_CLASSIFY_HEAD || mode > EI_CLASSIFY_SEGMENT) return EI_ERR_SHAPE;
-  if (!(probe_scale == probe_scale) || !(softmax_scale == softmax_scale)) return EI_ERR_SHAPE;
+  if (!probe_scale_ok(probe_scale) || !scale_ok(softmax_scale)) return EI_ERR_SHAPE;
   if (kmax < kmax_of(tiling, params)) return EI_ERR_SHAPE;
   if (!stream_aux || stream_aux == stream) return EI_ERR_SHAPE;
   const Sizes z = sizes(dims, &tiling);
@@ -251,6 +259,7 @@ ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const 
   // run the three stages over all heads on `stream` (the workspace then
   // covers all heads, else one group).
   const bool pipelined = z.N >= kPipelineMinTokens;
+  if (pipelined && !event) return EI_ERR_NULL;
   const ei::ProbeShape ps{1, G, 1, (int)z.N, tiling.seg_len, tiling.block_len, (int)z.CS,
                           (int)z.CB, (int)z.r};
   const ei::ProbeShape ps_all{(int)z.B, (int)z.Hq, (int)z.Hkv, (int)z.N, tiling.seg_len,
@@ -281,11 +290,11 @@ ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const 
   const int64_t n_groups = z.B * z.Hkv;
   const size_t qkv = (size_t)z.N * ei::kHeadDim;   // elements per head
   hipError_t err = hipSuccess;
-  // One event, re-recorded: a stream wait takes the record current when the
-  // wait is enqueued.  sb first waits for everything already queued on sa.
-  hipEvent_t ev = nullptr;
+  // The caller's event, re-recorded: a stream wait takes the record current
+  // when the wait is enqueued.  sb first waits for everything already queued
+  // on sa.
+  hipEvent_t ev = (hipEvent_t)event;
   if (pipelined) {
-    if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) return EI_ERR_LAUNCH;
     if ((err = hipEventRecord(ev, sa)) == hipSuccess) err = hipStreamWaitEvent(sb, ev, 0);
   }
   if (!pipelined) {
@@ -317,7 +326,6 @@ ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const 
   // sa waits for the last work on sb
   if (err == hipSuccess) err = hipEventRecord(ev, sb);
   if (err == hipSuccess) err = hipStreamWaitEvent(sa, ev, 0);
-  (void)hipEventDestroy(ev);   // released once its last record has completed
   return from_hip(err);
 }
 
@@ -326,7 +334,7 @@ ei_status ei_dense_prefill_attn(const uint16_t* q, const uint16_t* k, const uint
                                 void* stream) {
   ei_status st = check_dims(dims);
   if (st != EI_OK) return st;
-  if (!(softmax_scale == softmax_scale)) return EI_ERR_SHAPE;
+  if (!scale_ok(softmax_scale)) return EI_ERR_SHAPE;
   const Sizes z = sizes(dims, nullptr);
   if (z.B == 0 || z.N == 0) return EI_OK;
   if (!q || !k || !v || !o) return EI_ERR_NULL;

@@ -93,15 +93,31 @@ int main() {
   // the one-call path
   const size_t pws = ei_prefill_workspace_bytes(d, t);
   EXPECT(ei_entropy_guided_prefill(F16, F16, F16, d, t, 1.0, p, 0, km, 0.088f, FF, FF, FU, FI,
-                                   FI, FI, F16, FV, pws, FS, nullptr) == EI_ERR_SHAPE);
+                                   FI, FI, F16, FV, pws, FS, nullptr, FV) == EI_ERR_SHAPE);
   EXPECT(ei_entropy_guided_prefill(F16, F16, F16, d, t, 1.0, p, 0, km, 0.088f, FF, FF, FU, FI,
-                                   FI, FI, F16, FV, pws, FS, FS) == EI_ERR_SHAPE);
+                                   FI, FI, F16, FV, pws, FS, FS, FV) == EI_ERR_SHAPE);
   EXPECT(ei_entropy_guided_prefill(F16, F16, F16, d, t, 1.0, p, 0, km, 0.088f, FF, FF, FU, FI,
-                                   FI, FI, F16, FV, pws - 1, FS, FV) == EI_ERR_WORKSPACE);
+                                   FI, FI, F16, FV, pws - 1, FS, FV, FV) == EI_ERR_WORKSPACE);
   EXPECT(ei_entropy_guided_prefill(F16, F16, F16, d, t, 1.0, p, 7, km, 0.088f, FF, FF, FU, FI,
-                                   FI, FI, F16, FV, pws, FS, FV) == EI_ERR_SHAPE);
+                                   FI, FI, F16, FV, pws, FS, FV, FV) == EI_ERR_SHAPE);
   EXPECT(ei_entropy_guided_prefill(F16, F16, nullptr, d, t, 1.0, p, 0, km, 0.088f, FF, FF, FU,
-                                   FI, FI, FI, F16, FV, pws, FS, FV) == EI_ERR_NULL);
+                                   FI, FI, FI, F16, FV, pws, FS, FV, FV) == EI_ERR_NULL);
+
+  // scales: softmax_scale finite and > 0, probe_scale finite
+  for (float sc : {0.0f, -0.088f, INFINITY, -INFINITY, NAN}) {
+    EXPECT(ei_sparse_prefill_attn(F16, F16, F16, d, t, sc, FI, FI, km, F16, nullptr) ==
+           EI_ERR_SHAPE);
+    EXPECT(ei_dense_prefill_attn(F16, F16, F16, d, sc, 0, F16, nullptr) == EI_ERR_SHAPE);
+    EXPECT(ei_entropy_guided_prefill(F16, F16, F16, d, t, 1.0, p, 0, km, sc, FF, FF, FU, FI, FI,
+                                     FI, F16, FV, pws, FS, FV, FV) == EI_ERR_SHAPE);
+  }
+  for (double ps : {(double)INFINITY, (double)NAN})
+    EXPECT(ei_entropy_probe(F16, F16, d, t, ps, FF, FF, FV, ws, nullptr) == EI_ERR_SHAPE);
+  // the pipelined regime needs the caller's event
+  const ei_dims dl{1, 4, 1, 16384, 128};
+  EXPECT(ei_entropy_guided_prefill(F16, F16, F16, dl, t, 1.0, p, 0, km, 0.088f, FF, FF, FU, FI,
+                                   FI, FI, F16, FV, ei_prefill_workspace_bytes(dl, t), FS, FV,
+                                   nullptr) == EI_ERR_NULL);
 
   std::printf("abi sanitized run: %s\n", failures ? "FAILED" : "ok");
   return failures ? 1 : 0;

@@ -35,7 +35,7 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_helpers(L):
-    assert L.ei_abi_version() == 3
+    assert L.ei_abi_version() == 4
     assert eb.kmax(128, 64, 2048, 3) == 98
     assert eb.kmax(2048, 64, 2048, 3) == 96 + 32
     assert eb.kmax(256, 128, 256, 3) == 6 + 2
@@ -53,14 +53,18 @@ def test_helpers(L):
 
 FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: every call below fails validation
 FAKE2 = ctypes.c_void_p(0x2000)  # a second fake handle (stream)
+FAKE3 = ctypes.c_void_p(0x3000)  # a fake event handle
 
 
 @pytest.mark.parametrize("dims,tiling,expect", [
     (eb.Dims(1, 4, 1, 1024, 64), eb.Tiling(128, 64), -3),     # D != 128
     (eb.Dims(1, 6, 4, 1024, 128), eb.Tiling(128, 64), -2),    # Hq % Hkv
     (eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(128, 32), -3),    # L_B not 64/128
-    (eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(192, 64), -3),    # L_S not a multiple of 128
-    (eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(128, 256), -3),
+    (eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(192, 64), -2),    # L_S not a multiple of 128
+    (eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(128, 256), -3),   # L_B not 64/128
+    (eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(64, 64), -2),     # L_S below 128
+    (eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(0, 64), -2),
+    (eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(-128, 64), -2),
     (eb.Dims(-1, 4, 1, 1024, 128), eb.Tiling(128, 64), -2),
     (eb.Dims(1, 0, 1, 1024, 128), eb.Tiling(128, 64), -2),
 ])
@@ -129,15 +133,16 @@ def test_pipelined_prefill_rejects_bad_arguments(L):
     assert ws > 0 and ws == L.ei_probe_workspace_bytes(eb.Dims(1, 4, 1, 1024, 128), t)
     outs = (FAKE,) * 7
     call = L.ei_entropy_guided_prefill
-    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, FAKE, ws, FAKE, None) == -2
-    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, FAKE, ws, FAKE, FAKE) == -2
-    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 5, km, 0.088, *outs, FAKE, ws, FAKE, FAKE2) == -2
+    args = (FAKE, FAKE, FAKE, d, t, 1.0, p)
+    assert call(*args, 0, km, 0.088, *outs, FAKE, ws, FAKE, None, FAKE3) == -2
+    assert call(*args, 0, km, 0.088, *outs, FAKE, ws, FAKE, FAKE, FAKE3) == -2
+    assert call(*args, 5, km, 0.088, *outs, FAKE, ws, FAKE, FAKE2, FAKE3) == -2
     assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km - 1, 0.088, *outs, FAKE, ws, FAKE,
-                FAKE2) == -2
+                FAKE2, FAKE3) == -2
     assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, FAKE, ws - 1, FAKE,
-                FAKE2) == -4
+                FAKE2, FAKE3) == -4
     assert call(None, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, FAKE, ws, FAKE,
-                FAKE2) == -1
+                FAKE2, FAKE3) == -1
 
 
 def test_prefill_workspace_follows_the_two_regimes(L):
@@ -159,7 +164,7 @@ def test_prefill_workspace_follows_the_two_regimes(L):
     assert ws_one < L.ei_prefill_workspace_bytes(d, t)
     outs = (FAKE,) * 7
     assert L.ei_entropy_guided_prefill(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, FAKE,
-                                       ws_one, FAKE, FAKE2) == -4
+                                       ws_one, FAKE, FAKE2, FAKE3) == -4
 
 
 def test_bench_refuses_several_gpus():
@@ -229,12 +234,13 @@ def test_misaligned_pointers_are_refused(L):
     call = L.ei_entropy_guided_prefill
     outs = [FAKE] * 7
     assert call(FAKE, FAKE, _off(FAKE, 2), d, t, 1.0, p, 0, km, 0.088, *outs, FAKE, ws, FAKE,
-                FAKE2) == -3
+                FAKE2, FAKE3) == -3
     bad = list(outs)
     bad[4] = _off(FAKE, 2)   # block_idx
-    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *bad, FAKE, ws, FAKE, FAKE2) == -3
+    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *bad, FAKE, ws, FAKE, FAKE2,
+                FAKE3) == -3
     assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, _off(FAKE, 8), ws, FAKE,
-                FAKE2) == -3
+                FAKE2, FAKE3) == -3
 
 
 def test_sizes_whose_grids_overflow_are_refused(L):
@@ -292,3 +298,47 @@ def test_bench_counter_figures_are_scoped():
         assert (good is not None) == (f"attn_source_hash: {cur}" in txt)
         open(p, "w").write(txt.replace("attn_source_hash:", "attn_source_hash: 0"))
         assert bench.read_counter_file(p, "hbm_bytes_per_launch") is None
+
+
+BAD_SCALES = (0.0, -0.088, float("inf"), float("-inf"), float("nan"))
+
+
+@pytest.mark.parametrize("scale", BAD_SCALES)
+def test_attention_refuses_non_positive_or_non_finite_scales(L, scale):
+    """The kernels mask scores before scaling and take the maximum of the raw
+    scores, which is the maximum of the scaled ones only for a positive scale:
+    every attention entry point (and the one-call path) refuses a
+    softmax_scale that is not finite and > 0 before any launch."""
+    d, t = eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(128, 64)
+    km = 98
+    assert L.ei_sparse_prefill_attn(FAKE, FAKE, FAKE, d, t, scale, FAKE, FAKE, km, FAKE,
+                                    None) == -2
+    assert L.ei_sparse_prefill_attn_gqa_union(FAKE, FAKE, FAKE, d, t, scale, FAKE, FAKE, km,
+                                              FAKE, None) == -2
+    for causal in (0, 1):
+        assert L.ei_dense_prefill_attn(FAKE, FAKE, FAKE, d, scale, causal, FAKE, None) == -2
+    p = eb.budget_params()
+    ws = L.ei_prefill_workspace_bytes(d, t)
+    assert L.ei_entropy_guided_prefill(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, L.ei_kmax(t, p), scale,
+                                       *(FAKE,) * 7, FAKE, ws, FAKE, FAKE2, FAKE3) == -2
+
+
+@pytest.mark.parametrize("ps", (float("inf"), float("-inf"), float("nan")))
+def test_probe_refuses_non_finite_probe_scale(L, ps):
+    d, t = eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(128, 64)
+    need = L.ei_probe_workspace_bytes(d, t)
+    assert L.ei_entropy_probe(FAKE, FAKE, d, t, ps, FAKE, FAKE, FAKE, need, None) == -2
+    p = eb.budget_params()
+    ws = L.ei_prefill_workspace_bytes(d, t)
+    assert L.ei_entropy_guided_prefill(FAKE, FAKE, FAKE, d, t, ps, p, 0, L.ei_kmax(t, p), 0.088,
+                                       *(FAKE,) * 7, FAKE, ws, FAKE, FAKE2, FAKE3) == -2
+
+
+def test_pipelined_prefill_needs_an_event(L):
+    """From 16384 tokens on the one-call path orders its two streams with the
+    caller's event: a NULL event is EI_ERR_NULL before any launch."""
+    t, p = eb.Tiling(128, 64), eb.budget_params()
+    d = eb.Dims(1, 4, 1, 16384, 128)
+    ws = L.ei_prefill_workspace_bytes(d, t)
+    assert L.ei_entropy_guided_prefill(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, L.ei_kmax(t, p), 0.088,
+                                       *(FAKE,) * 7, FAKE, ws, FAKE, FAKE2, None) == -1
