@@ -37,8 +37,9 @@
  *    EI_ERR_UNSUPPORTED.
  *  - Outputs must not alias inputs.  Identical inputs give bitwise-identical
  *    outputs (the only atomics are integer counts in LDS, whose order does
- *    not matter).  No global state, no logging; calls on different streams
- *    may run concurrently.
+ *    not matter).  No global state (except the no-allocation variant's
+ *    scratch array), no logging; calls on different streams may run
+ *    concurrently.
  */
 #ifndef ENTROPYINFER_H
 #define ENTROPYINFER_H
@@ -299,6 +300,34 @@ ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const 
                                     int32_t* block_idx, int32_t* block_cnt, uint16_t* o,
                                     void* workspace, size_t workspace_bytes, void* stream,
                                     void* stream_aux, void* event);
+
+/* Device scratch that ei_entropy_guided_prefill_noalloc holds on every device
+ * it runs on, until the process ends (32 MiB). */
+#define EI_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+
+/*
+ * ei_entropy_guided_prefill_noalloc -- ei_entropy_guided_prefill for callers
+ * that cannot allocate device memory: work captured into a HIP graph, tight
+ * serving loops, harnesses that forbid hipMalloc.  The same arguments and
+ * bitwise the same outputs, without the workspace: the probe workspace is a
+ * static device array of EI_NOALLOC_SCRATCH_BYTES per device (looked up on the
+ * first call on a device, with that device current).  The call allocates and
+ * frees nothing.  Every call on a device shares that device's array, so calls
+ * that overlap on one device (on different streams, or from several threads)
+ * race and must be serialised by the caller.
+ *
+ * Errors: those of ei_entropy_guided_prefill; EI_ERR_WORKSPACE when the
+ * problem needs more than EI_NOALLOC_SCRATCH_BYTES (ei_prefill_workspace_bytes
+ * tells), EI_ERR_LAUNCH if the scratch array's address cannot be looked up.
+ */
+ei_status ei_entropy_guided_prefill_noalloc(const uint16_t* q, const uint16_t* k,
+                                            const uint16_t* v, ei_dims dims, ei_tiling tiling,
+                                            double probe_scale, ei_budget_params params,
+                                            int32_t mode, int32_t kmax, float softmax_scale,
+                                            float* log_scores, float* entropy,
+                                            uint8_t* head_is_rigid, int32_t* budget_blocks,
+                                            int32_t* block_idx, int32_t* block_cnt, uint16_t* o,
+                                            void* stream, void* stream_aux, void* event);
 
 #ifdef __cplusplus
 }

@@ -86,6 +86,10 @@ def lib() -> ctypes.CDLL:
                                                 BudgetParams, ctypes.c_int32, ctypes.c_int32,
                                                 ctypes.c_float, _VP, _VP, _VP, _VP, _VP, _VP,
                                                 _VP, _VP, ctypes.c_size_t, _VP, _VP, _VP]
+        L.ei_entropy_guided_prefill_noalloc.restype = ctypes.c_int
+        L.ei_entropy_guided_prefill_noalloc.argtypes = [
+            _VP, _VP, _VP, Dims, Tiling, ctypes.c_double, BudgetParams, ctypes.c_int32,
+            ctypes.c_int32, ctypes.c_float, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP]
         L.ei_sparse_prefill_attn_gqa_union.restype = ctypes.c_int
         L.ei_sparse_prefill_attn_gqa_union.argtypes = L.ei_sparse_prefill_attn.argtypes
         L.ei_dense_prefill_attn.restype = ctypes.c_int
@@ -336,12 +340,14 @@ def entropy_guided_prefill(q, k, v, seg_len: int = 128, block_len: int = 64,
                            base_budget: int = 2048, e_t: float = 1e-5, alpha: float = 0.5,
                            delta_t: float = 0.4, mult: int = 3, probe_scale: float = 1.0,
                            softmax_scale: float | None = None, bufs: dict | None = None,
-                           mode: int = CLASSIFY_HEAD):
+                           mode: int = CLASSIFY_HEAD, noalloc: bool = False):
     """ei_entropy_guided_prefill: the whole path on one layer (probe -> select
     -> sparse attention), pipelined over KV-head groups on the current stream
     and a second stream.  ``bufs`` (optional) caches the output and scratch
     buffers between calls.  Returns (output, selection dict, log_scores,
-    entropy)."""
+    entropy).  With ``noalloc`` the call goes to
+    ei_entropy_guided_prefill_noalloc (no workspace: the library's static
+    scratch array)."""
     for t, n in ((q, "q"), (k, "k"), (v, "v")):
         _req(t, n, torch.bfloat16, 4)
     check_qkv_shapes(q.shape, k.shape, v.shape)
@@ -360,22 +366,27 @@ def entropy_guided_prefill(q, k, v, seg_len: int = 128, block_len: int = 64,
         t = bufs.get(name)
         if t is None or tuple(t.shape) != shape or t.dtype != dtype or t.device != dev:
             bufs[name] = torch.empty(shape, dtype=dtype, device=dev)
-    need = max(prefill_workspace_bytes(d, seg_len, block_len), 1)
-    ws = bufs.get("workspace")
-    if ws is None or ws.numel() < need or ws.device != dev:
-        bufs["workspace"] = ws = torch.empty((need,), dtype=torch.uint8, device=dev)
+    if not noalloc:
+        need = max(prefill_workspace_bytes(d, seg_len, block_len), 1)
+        ws = bufs.get("workspace")
+        if ws is None or ws.numel() < need or ws.device != dev:
+            bufs["workspace"] = ws = torch.empty((need,), dtype=torch.uint8, device=dev)
     scale = (1.0 / math.sqrt(D)) if softmax_scale is None else float(softmax_scale)
     aux = _aux_stream(dev)
     ev = _order_event(dev)
-    with torch.cuda.device(dev):
-        st = lib().ei_entropy_guided_prefill(
-            _ptr(q), _ptr(k), _ptr(v), d, Tiling(seg_len, block_len), float(probe_scale),
+    args = (_ptr(q), _ptr(k), _ptr(v), d, Tiling(seg_len, block_len), float(probe_scale),
             budget_params(e_t, alpha, delta_t, base_budget, mult), int(mode), km, scale,
             _ptr(bufs["log_scores"]), _ptr(bufs["entropy"]), _ptr(bufs["rigid"]),
-            _ptr(bufs["budget"]), _ptr(bufs["idx"]), _ptr(bufs["cnt"]), _ptr(bufs["out"]),
-            _ptr(ws), ws.numel(), _stream(q), ctypes.c_void_p(aux.cuda_stream),
-            ctypes.c_void_p(ev.cuda_event))
-    _check("ei_entropy_guided_prefill", st)
+            _ptr(bufs["budget"]), _ptr(bufs["idx"]), _ptr(bufs["cnt"]), _ptr(bufs["out"]))
+    streams = (_stream(q), ctypes.c_void_p(aux.cuda_stream), ctypes.c_void_p(ev.cuda_event))
+    with torch.cuda.device(dev):
+        if noalloc:
+            fn = "ei_entropy_guided_prefill_noalloc"
+            st = lib().ei_entropy_guided_prefill_noalloc(*args, *streams)
+        else:
+            fn = "ei_entropy_guided_prefill"
+            st = lib().ei_entropy_guided_prefill(*args, _ptr(ws), ws.numel(), *streams)
+    _check(fn, st)
     # keep the buffers alive until the auxiliary stream's work has used them
     for t in list(bufs.values()) + [q, k, v]:
         if isinstance(t, torch.Tensor):

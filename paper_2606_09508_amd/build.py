@@ -16,7 +16,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libentropyinfer.so")
 ROOT = os.path.dirname(HERE)
 
-SOURCES = ["ei_api.hip", "ei_probe.hip", "ei_select.hip", "ei_attn.hip"]
+SOURCES = ["ei_api.hip", "ei_probe.hip", "ei_select.hip", "ei_attn.hip", "ei_noalloc.hip"]
 ARCH = os.environ.get("EI_OFFLOAD_ARCH", "gfx950")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

@@ -342,3 +342,25 @@ def test_pipelined_prefill_needs_an_event(L):
     ws = L.ei_prefill_workspace_bytes(d, t)
     assert L.ei_entropy_guided_prefill(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, L.ei_kmax(t, p), 0.088,
                                        *(FAKE,) * 7, FAKE, ws, FAKE, FAKE2, None) == -1
+
+
+def test_noalloc_prefill_refusals(L):
+    """ei_entropy_guided_prefill_noalloc validates like the workspace entry
+    point and refuses, before touching a device, a problem whose probe
+    workspace exceeds its static scratch array (32 MiB)."""
+    t, p = eb.Tiling(128, 64), eb.budget_params()
+    km = L.ei_kmax(t, p)
+    call = L.ei_entropy_guided_prefill_noalloc
+    outs = (FAKE,) * 7
+    big = eb.Dims(1, 64, 1, 131072, 128)   # one KV group of 64 heads at 128k
+    assert L.ei_prefill_workspace_bytes(big, t) > 32 << 20
+    assert call(FAKE, FAKE, FAKE, big, t, 1.0, p, 0, km, 0.088, *outs, FAKE, FAKE2, FAKE3) == -4
+    d = eb.Dims(1, 4, 1, 16384, 128)
+    assert L.ei_prefill_workspace_bytes(d, t) <= 32 << 20
+    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.0, *outs, FAKE, FAKE2, FAKE3) == -2
+    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, FAKE, FAKE2, None) == -1
+    assert call(None, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, FAKE, FAKE2, FAKE3) == -1
+    assert call(FAKE, FAKE, FAKE, eb.Dims(1, 4, 1, 1024, 96), t, 1.0, p, 0, km, 0.088, *outs,
+                FAKE, FAKE2, FAKE3) == -3
+    assert call(None, None, None, eb.Dims(0, 4, 1, 1024, 128), t, 1.0, p, 0, km, 0.088,
+                *(None,) * 7, FAKE, FAKE2, None) == 0

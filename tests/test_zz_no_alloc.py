@@ -1,0 +1,57 @@
+"""ei_entropy_guided_prefill_noalloc (the one-call path with the library's
+static scratch array instead of a caller's workspace) against
+ei_entropy_guided_prefill on the same inputs, bitwise, through the C ABI: two
+calls in a row, the second on a smaller problem (so the scratch array holds
+the first call's larger contents when the second runs), and the pipelined
+and the short regimes both covered."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_09508_amd import binding as eb
+from paper_2606_09508_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+def to_dev(a: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def run(w, noalloc):
+    q, k, v = to_dev(w.q), to_dev(w.k), to_dev(w.v)
+    o, sel, ls, en = eb.entropy_guided_prefill(q, k, v, w.Ls, w.Lb, w.base_budget, w.e_t, w.alpha,
+                                               w.delta_t, w.mult, w.probe_scale, w.softmax_scale,
+                                               noalloc=noalloc)
+    torch.cuda.synchronize()
+    return o.clone(), {n: t.clone() for n, t in sel.items()}, ls.clone(), en.clone()
+
+
+def same(w, a, b):
+    oa, sa, la, ea = a
+    ob, sb, lb, eb_ = b
+    assert torch.equal(oa, ob)
+    assert torch.equal(ea, eb_)
+    for name in ("rigid", "budget", "idx", "cnt"):
+        assert torch.equal(sa[name], sb[name]), name
+    r = w.Ls // w.Lb
+    for s in range(w.CS):   # ln A is defined on the visible blocks only
+        nv = min((s + 1) * r, w.CB)
+        assert torch.equal(la[:, :, s, :nv], lb[:, :, s, :nv])
+
+
+def test_noalloc_equals_workspace_entry_point_two_calls():
+    """Collected last (test_zz_*): it also passes after every other GPU test
+    has run in the same process."""
+    cases = [("c2", 1, dict(N=32768)),          # pipelined over KV-head groups
+             ("c1", 3, dict(Hq=8, Hkv=2, N=4096 + 192))]   # smaller, short regime
+    for wl, seed, case in cases:
+        w = synth.make(wl, seed, **case)
+        print(f"[noalloc] {wl} seed={seed} {case}", file=sys.stderr, flush=True)
+        ref = run(w, noalloc=False)
+        got = run(w, noalloc=True)
+        same(w, ref, got)
+        again = run(w, noalloc=True)   # the array now holds this call's own data
+        same(w, ref, again)
