@@ -7,9 +7,9 @@ Llama-3-8B attention layer at 131072 tokens (Hq=32, Hkv=8, D=128, L_S=128,
 L_B=64, B_h=2048).  Prints one JSON line; see the keys below.
 
 ``value`` / ``ms_per_step`` time the library's one-call path for the layer
-(ei_entropy_guided_prefill: the stages pipelined over KV-head groups on two
-streams); ``stages_ms`` and ``serial_ms_per_step`` time the three separate
-calls on one stream, whose sparse-attention launch gives the roofline.
+(ei_entropy_guided_prefill: the three stages in one call); ``stages_ms`` and
+``serial_ms_per_step`` time the three separate calls on one stream, whose
+sparse-attention launch gives the roofline.
 """
 from __future__ import annotations
 
@@ -215,8 +215,8 @@ def main():
     probe_ms, select_ms, sparse_ms = [float(x) for x in st.mean(axis=0)]
     pct = np.percentile(st, [10, 50, 90], axis=0)
 
-    # the product's step: ei_entropy_guided_prefill, the same three stages
-    # pipelined over KV-head groups on two streams (bitwise the same outputs)
+    # the product's step: ei_entropy_guided_prefill, the same three stages in
+    # one call (bitwise the same outputs)
     pbufs = {}
 
     def pstep():
@@ -237,7 +237,7 @@ def main():
     pipe_all = np.array([e[0].elapsed_time(e[1]) for e in pev])
     pipe_ms = float(pipe_all.mean())
     if not torch.equal(pbufs["out"], bufs["out"]):
-        print("pipelined output differs from the separate calls", file=sys.stderr)
+        print("the one-call output differs from the separate calls", file=sys.stderr)
         sys.exit(1)
 
     # probe and select with cold caches: a 512 MB write evicts L2 and MALL

@@ -112,8 +112,9 @@ int64_t ei_num_blocks(ei_dims dims, ei_tiling tiling);
  * floor(mult * B_h / L_B) + L_S / L_B; -1 on invalid parameters. */
 int32_t ei_kmax(ei_tiling tiling, ei_budget_params params);
 
-/* Workspace bytes ei_entropy_probe needs (Q representation in binary64 and
- * K representation in fp32, Algorithm 1); 0 on invalid sizes. */
+/* Workspace bytes ei_entropy_probe needs (the pooled Q and K representation
+ * vectors of Algorithm 1 as fixed-point limbs, residual parts and scales);
+ * 0 on invalid sizes. */
 size_t ei_probe_workspace_bytes(ei_dims dims, ei_tiling tiling);
 
 /*
@@ -123,8 +124,11 @@ size_t ei_probe_workspace_bytes(ei_dims dims, ei_tiling tiling);
  * min((s+1) r, C_B) (block-causal, including the segment's own blocks):
  * Q_max / Q_min are the element-wise max / min of the segment's query rows,
  * K_max / K_min those of the block's key rows (Algorithm 1); the four logits
- * x_ab = probe_scale * <Q_a, K_b> are computed in binary64 (exact for bf16
- * products); S1..S4 are their softmaxes over j; A = max((S1 + S2) / 2,
+ * x_ab = probe_scale * <Q_a, K_b> are formed exactly as integer dot products
+ * of 7-bit limbs of the vectors' fixed-point forms (int8 matrix cores), plus
+ * the products of the parts below the fixed-point grid where those can move
+ * a logit by 2^-30 or more, in binary64; S1..S4 are their softmaxes over j;
+ * A = max((S1 + S2) / 2,
  * (S3 + S4) / 2) (Algorithm 2, used without renormalisation); the entropy is
  * -sum_j A ln A (natural log, Section 3).
  *
@@ -135,8 +139,11 @@ size_t ei_probe_workspace_bytes(ei_dims dims, ei_tiling tiling);
  *   entropy      out, fp32 [B][Hq][C_S]
  *   workspace    device scratch of at least ei_probe_workspace_bytes()
  *
- * Errors: EI_ERR_NULL, EI_ERR_SHAPE, EI_ERR_UNSUPPORTED (D != 128, or C_B too
- * large for one workgroup's LDS), EI_ERR_WORKSPACE, EI_ERR_LAUNCH.
+ * A non-finite element of Q or K makes every logit it enters, and so its
+ * rows' ln A and entropy, NaN.
+ *
+ * Errors: EI_ERR_NULL, EI_ERR_SHAPE, EI_ERR_UNSUPPORTED (D != 128),
+ * EI_ERR_WORKSPACE, EI_ERR_LAUNCH.
  */
 ei_status ei_entropy_probe(const uint16_t* q, const uint16_t* k, ei_dims dims,
                            ei_tiling tiling, double probe_scale, float* log_scores,
@@ -254,21 +261,15 @@ ei_status ei_dense_prefill_attn(const uint16_t* q, const uint16_t* k, const uint
                                 ei_dims dims, float softmax_scale, int32_t causal,
                                 uint16_t* o, void* stream);
 
-/* Workspace bytes ei_entropy_guided_prefill needs (the probe workspace of
- * one KV-head group, reused group after group); 0 on invalid sizes. */
+/* Workspace bytes ei_entropy_guided_prefill needs (= ei_probe_workspace_bytes);
+ * 0 on invalid sizes. */
 size_t ei_prefill_workspace_bytes(ei_dims dims, ei_tiling tiling);
 
 /*
  * ei_entropy_guided_prefill -- the whole prefill path of one layer (Section
- * 4.2): ei_entropy_probe, ei_select_blocks_mode and ei_sparse_prefill_attn for
- * every head.  From N = 16384 tokens on the stages are pipelined over
- * (batch, KV-head group): the probe of group g+1 runs on `stream` while the
- * selection and sparse attention of group g run on `stream_aux`.  Below that
- * the per-group launches cost more than the overlap gains, and the call runs
- * the probes group by group, then one selection and one attention launch over
- * all heads, on `stream` alone.  Every kernel sees exactly the data it would
- * see in the three separate calls, so all outputs are bitwise identical to
- * them either way.
+ * 4.2): ei_entropy_probe, ei_select_blocks_mode and ei_sparse_prefill_attn
+ * over all heads, in this order on `stream`, with the arguments validated
+ * once for all three.  The outputs are bitwise those of the three calls.
  *
  *   q, k, v            as ei_sparse_prefill_attn
  *   probe_scale        as ei_entropy_probe; softmax_scale as the attention
@@ -276,21 +277,8 @@ size_t ei_prefill_workspace_bytes(ei_dims dims, ei_tiling tiling);
  *   log_scores, entropy, head_is_rigid, budget_blocks, block_idx, block_cnt,
  *   o                  outputs of the three calls (same layouts)
  *   workspace          at least ei_prefill_workspace_bytes()
- *   stream, stream_aux hipStream_t, distinct (NULL = the default stream is
- *                      allowed for `stream` only).  On return `stream` is
- *                      ordered after all the work: synchronising `stream`
- *                      makes every output valid.  Both streams must be of
- *                      default priority.
- *   event              a hipEvent_t created by the caller (any flags;
- *                      hipEventDisableTiming is the cheapest) on the device
- *                      of the streams; the call records it on both streams to
- *                      order them, so it must not be in use by concurrent
- *                      work.  Required from N = 16384 tokens on (the
- *                      pipelined regime); may be NULL below.
  *
- * Errors: those of the three calls, plus EI_ERR_SHAPE if stream_aux is NULL
- * or equal to stream, EI_ERR_NULL if the pipelined regime has no event, and
- * EI_ERR_LAUNCH if an event record or stream wait fails.
+ * Errors: those of the three calls.
  */
 ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                                     ei_dims dims, ei_tiling tiling, double probe_scale,
@@ -298,12 +286,12 @@ ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const 
                                     float softmax_scale, float* log_scores, float* entropy,
                                     uint8_t* head_is_rigid, int32_t* budget_blocks,
                                     int32_t* block_idx, int32_t* block_cnt, uint16_t* o,
-                                    void* workspace, size_t workspace_bytes, void* stream,
-                                    void* stream_aux, void* event);
+                                    void* workspace, size_t workspace_bytes, void* stream);
 
 /* Device scratch that ei_entropy_guided_prefill_noalloc holds on every device
- * it runs on, until the process ends (32 MiB). */
-#define EI_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+ * it runs on, until the process ends (128 MiB: the probe workspace of a layer
+ * of 64 query and 8 KV heads at 131072 tokens is 123 MiB). */
+#define EI_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
 
 /*
  * ei_entropy_guided_prefill_noalloc -- ei_entropy_guided_prefill for callers
@@ -327,7 +315,7 @@ ei_status ei_entropy_guided_prefill_noalloc(const uint16_t* q, const uint16_t* k
                                             float* log_scores, float* entropy,
                                             uint8_t* head_is_rigid, int32_t* budget_blocks,
                                             int32_t* block_idx, int32_t* block_cnt, uint16_t* o,
-                                            void* stream, void* stream_aux, void* event);
+                                            void* stream);
 
 #ifdef __cplusplus
 }

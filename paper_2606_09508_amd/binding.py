@@ -85,11 +85,11 @@ def lib() -> ctypes.CDLL:
         L.ei_entropy_guided_prefill.argtypes = [_VP, _VP, _VP, Dims, Tiling, ctypes.c_double,
                                                 BudgetParams, ctypes.c_int32, ctypes.c_int32,
                                                 ctypes.c_float, _VP, _VP, _VP, _VP, _VP, _VP,
-                                                _VP, _VP, ctypes.c_size_t, _VP, _VP, _VP]
+                                                _VP, _VP, ctypes.c_size_t, _VP]
         L.ei_entropy_guided_prefill_noalloc.restype = ctypes.c_int
         L.ei_entropy_guided_prefill_noalloc.argtypes = [
             _VP, _VP, _VP, Dims, Tiling, ctypes.c_double, BudgetParams, ctypes.c_int32,
-            ctypes.c_int32, ctypes.c_float, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP]
+            ctypes.c_int32, ctypes.c_float, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP]
         L.ei_sparse_prefill_attn_gqa_union.restype = ctypes.c_int
         L.ei_sparse_prefill_attn_gqa_union.argtypes = L.ei_sparse_prefill_attn.argtypes
         L.ei_dense_prefill_attn.restype = ctypes.c_int
@@ -308,30 +308,6 @@ def dense_prefill_attn(q, k, v, softmax_scale: float | None = None, causal: bool
     return out
 
 
-_AUX_STREAMS: dict = {}
-_EVENTS: dict = {}
-
-
-def _aux_stream(device) -> torch.cuda.Stream:
-    """A second stream per device (default priority) for the pipelined path."""
-    idx = torch.device(device).index or 0
-    if idx not in _AUX_STREAMS:
-        _AUX_STREAMS[idx] = torch.cuda.Stream(device=idx)
-    return _AUX_STREAMS[idx]
-
-
-def _order_event(device) -> torch.cuda.Event:
-    """The event the pipelined path uses to order its two streams, one per
-    device, created once (torch creates the HIP event on its first record)."""
-    idx = torch.device(device).index or 0
-    if idx not in _EVENTS:
-        ev = torch.cuda.Event()
-        with torch.cuda.device(idx):
-            ev.record(torch.cuda.current_stream(idx))
-        _EVENTS[idx] = ev
-    return _EVENTS[idx]
-
-
 def prefill_workspace_bytes(dims: Dims, seg_len: int, block_len: int) -> int:
     return int(lib().ei_prefill_workspace_bytes(dims, Tiling(seg_len, block_len)))
 
@@ -342,10 +318,9 @@ def entropy_guided_prefill(q, k, v, seg_len: int = 128, block_len: int = 64,
                            softmax_scale: float | None = None, bufs: dict | None = None,
                            mode: int = CLASSIFY_HEAD, noalloc: bool = False):
     """ei_entropy_guided_prefill: the whole path on one layer (probe -> select
-    -> sparse attention), pipelined over KV-head groups on the current stream
-    and a second stream.  ``bufs`` (optional) caches the output and scratch
-    buffers between calls.  Returns (output, selection dict, log_scores,
-    entropy).  With ``noalloc`` the call goes to
+    -> sparse attention) on the current stream.  ``bufs`` (optional) caches
+    the output and scratch buffers between calls.  Returns (output, selection
+    dict, log_scores, entropy).  With ``noalloc`` the call goes to
     ei_entropy_guided_prefill_noalloc (no workspace: the library's static
     scratch array)."""
     for t, n in ((q, "q"), (k, "k"), (v, "v")):
@@ -372,24 +347,17 @@ def entropy_guided_prefill(q, k, v, seg_len: int = 128, block_len: int = 64,
         if ws is None or ws.numel() < need or ws.device != dev:
             bufs["workspace"] = ws = torch.empty((need,), dtype=torch.uint8, device=dev)
     scale = (1.0 / math.sqrt(D)) if softmax_scale is None else float(softmax_scale)
-    aux = _aux_stream(dev)
-    ev = _order_event(dev)
     args = (_ptr(q), _ptr(k), _ptr(v), d, Tiling(seg_len, block_len), float(probe_scale),
             budget_params(e_t, alpha, delta_t, base_budget, mult), int(mode), km, scale,
             _ptr(bufs["log_scores"]), _ptr(bufs["entropy"]), _ptr(bufs["rigid"]),
             _ptr(bufs["budget"]), _ptr(bufs["idx"]), _ptr(bufs["cnt"]), _ptr(bufs["out"]))
-    streams = (_stream(q), ctypes.c_void_p(aux.cuda_stream), ctypes.c_void_p(ev.cuda_event))
     with torch.cuda.device(dev):
         if noalloc:
             fn = "ei_entropy_guided_prefill_noalloc"
-            st = lib().ei_entropy_guided_prefill_noalloc(*args, *streams)
+            st = lib().ei_entropy_guided_prefill_noalloc(*args, _stream(q))
         else:
             fn = "ei_entropy_guided_prefill"
-            st = lib().ei_entropy_guided_prefill(*args, _ptr(ws), ws.numel(), *streams)
+            st = lib().ei_entropy_guided_prefill(*args, _ptr(ws), ws.numel(), _stream(q))
     _check(fn, st)
-    # keep the buffers alive until the auxiliary stream's work has used them
-    for t in list(bufs.values()) + [q, k, v]:
-        if isinstance(t, torch.Tensor):
-            t.record_stream(aux)
     sel = {n: bufs[n] for n in ("rigid", "budget", "idx", "cnt")}
     return bufs["out"], sel, bufs["log_scores"], bufs["entropy"]

@@ -10,10 +10,7 @@
 
 namespace {
 
-constexpr int32_t kAbiVersion = 4;
-
-// ei_entropy_guided_prefill pipelines over KV-head groups from this length on.
-constexpr int64_t kPipelineMinTokens = 16384;
+constexpr int32_t kAbiVersion = 5;
 
 struct Sizes {
   int64_t B, Hq, Hkv, N, D, CS, CB, r;
@@ -123,7 +120,7 @@ size_t ei_probe_workspace_bytes(ei_dims dims, ei_tiling tiling) {
   const Sizes z = sizes(dims, &tiling);
   const ei::ProbeShape ps{(int)z.B, (int)z.Hq, (int)z.Hkv, (int)z.N, tiling.seg_len,
                           tiling.block_len, (int)z.CS, (int)z.CB, (int)z.r};
-  return ei::probe_qrep_bytes(ps) + ei::probe_krep_bytes(ps);
+  return ei::probe_workspace_bytes(ps);
 }
 
 ei_status ei_entropy_probe(const uint16_t* q, const uint16_t* k, ei_dims dims, ei_tiling tiling,
@@ -140,7 +137,7 @@ ei_status ei_entropy_probe(const uint16_t* q, const uint16_t* k, ei_dims dims, e
   const ei::ProbeShape ps{(int)z.B, (int)z.Hq, (int)z.Hkv, (int)z.N, tiling.seg_len,
                           tiling.block_len, (int)z.CS, (int)z.CB, (int)z.r};
   if (!ei::probe_supported(ps)) return EI_ERR_UNSUPPORTED;
-  if (!workspace || workspace_bytes < ei::probe_qrep_bytes(ps) + ei::probe_krep_bytes(ps))
+  if (!workspace || workspace_bytes < ei::probe_workspace_bytes(ps))
     return EI_ERR_WORKSPACE;
   if (!aligned16({workspace})) return EI_ERR_UNSUPPORTED;
   return from_hip(ei::launch_probe(q, k, ps, probe_scale, log_scores, entropy, workspace,
@@ -219,14 +216,7 @@ ei_status ei_sparse_prefill_attn_gqa_union(const uint16_t* q, const uint16_t* k,
 }
 
 size_t ei_prefill_workspace_bytes(ei_dims dims, ei_tiling tiling) {
-  if (check_dims(dims) != EI_OK || check_tiling(tiling) != EI_OK) return 0;
-  // short sequences: one probe over all heads
-  if (dims.seq_len < kPipelineMinTokens) return ei_probe_workspace_bytes(dims, tiling);
-  ei_dims one = dims;   // one (batch, KV head) group
-  one.batch = dims.batch > 0 ? 1 : 0;
-  one.n_q_heads = dims.n_q_heads / dims.n_kv_heads;
-  one.n_kv_heads = 1;
-  return ei_probe_workspace_bytes(one, tiling);
+  return ei_probe_workspace_bytes(dims, tiling);
 }
 
 ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const uint16_t* v,
@@ -235,8 +225,7 @@ ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const 
                                     float softmax_scale, float* log_scores, float* entropy,
                                     uint8_t* head_is_rigid, int32_t* budget_blocks,
                                     int32_t* block_idx, int32_t* block_cnt, uint16_t* o,
-                                    void* workspace, size_t workspace_bytes, void* stream,
-                                    void* stream_aux, void* event) {
+                                    void* workspace, size_t workspace_bytes, void* stream) {
   // validate the whole problem as the three calls would
   ei_status st = check_dims(dims);
   if (st != EI_OK) return st;
@@ -245,7 +234,6 @@ ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const 
   if (mode < EI_CLASSIFY_HEAD || mode > EI_CLASSIFY_SEGMENT) return EI_ERR_SHAPE;
   if (!probe_scale_ok(probe_scale) || !scale_ok(softmax_scale)) return EI_ERR_SHAPE;
   if (kmax < kmax_of(tiling, params)) return EI_ERR_SHAPE;
-  if (!stream_aux || stream_aux == stream) return EI_ERR_SHAPE;
   const Sizes z = sizes(dims, &tiling);
   if (z.B == 0 || z.N == 0) return EI_OK;
   if (!q || !k || !v || !log_scores || !entropy || !head_is_rigid || !budget_blocks ||
@@ -254,78 +242,29 @@ ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const 
   if (!aligned16({q, k, v, o}) ||
       !aligned4({log_scores, entropy, budget_blocks, block_idx, block_cnt}))
     return EI_ERR_UNSUPPORTED;
-  const int G = (int)(z.Hq / z.Hkv);
-  // Short sequences: the per-group launches cost more than the overlap saves;
-  // run the three stages over all heads on `stream` (the workspace then
-  // covers all heads, else one group).
-  const bool pipelined = z.N >= kPipelineMinTokens;
-  if (pipelined && !event) return EI_ERR_NULL;
-  const ei::ProbeShape ps{1, G, 1, (int)z.N, tiling.seg_len, tiling.block_len, (int)z.CS,
-                          (int)z.CB, (int)z.r};
-  const ei::ProbeShape ps_all{(int)z.B, (int)z.Hq, (int)z.Hkv, (int)z.N, tiling.seg_len,
-                              tiling.block_len, (int)z.CS, (int)z.CB, (int)z.r};
-  const ei::ProbeShape& pw = pipelined ? ps : ps_all;
-  if (!ei::probe_supported(pw)) return EI_ERR_UNSUPPORTED;
-  if (!workspace || workspace_bytes < ei::probe_qrep_bytes(pw) + ei::probe_krep_bytes(pw))
-    return EI_ERR_WORKSPACE;
-  if (!aligned16({workspace})) return EI_ERR_UNSUPPORTED;
-  const ei::SelectShape ss{1, G, (int)z.N, tiling.seg_len, tiling.block_len, (int)z.CS,
-                           (int)z.CB, (int)z.r, kmax, params.entropy_threshold, params.alpha,
-                           params.delta_t, params.base_budget_tokens, params.max_budget_mult,
-                           (int)mode, G};
+  const ei::ProbeShape ps{(int)z.B, (int)z.Hq, (int)z.Hkv, (int)z.N, tiling.seg_len,
+                          tiling.block_len, (int)z.CS, (int)z.CB, (int)z.r};
+  if (!ei::probe_supported(ps)) return EI_ERR_UNSUPPORTED;
+  const ei::SelectShape ss{(int)z.B, (int)z.Hq, (int)z.N, tiling.seg_len, tiling.block_len,
+                           (int)z.CS, (int)z.CB, (int)z.r, kmax, params.entropy_threshold,
+                           params.alpha, params.delta_t, params.base_budget_tokens,
+                           params.max_budget_mult, (int)mode, (int)(z.Hq / z.Hkv)};
   if (!ei::select_supported(ss)) return EI_ERR_UNSUPPORTED;
-  const ei::AttnShape as{1, G, 1, (int)z.N, tiling.seg_len, tiling.block_len, (int)z.CS,
-                         (int)z.CB, kmax, softmax_scale};
-  // the same stages over all heads at once (short sequences)
-  const ei::SelectShape ss_all{(int)z.B, (int)z.Hq, (int)z.N, tiling.seg_len, tiling.block_len,
-                               (int)z.CS, (int)z.CB, (int)z.r, kmax, params.entropy_threshold,
-                               params.alpha, params.delta_t, params.base_budget_tokens,
-                               params.max_budget_mult, (int)mode, G};
-  const ei::AttnShape as_all{(int)z.B, (int)z.Hq, (int)z.Hkv, (int)z.N, tiling.seg_len,
-                             tiling.block_len, (int)z.CS, (int)z.CB, kmax, softmax_scale};
-  if (!pipelined && !ei::select_supported(ss_all)) return EI_ERR_UNSUPPORTED;
-
-  hipStream_t sa = (hipStream_t)stream;
-  hipStream_t sb = pipelined ? (hipStream_t)stream_aux : sa;
-  const int64_t n_groups = z.B * z.Hkv;
-  const size_t qkv = (size_t)z.N * ei::kHeadDim;   // elements per head
-  hipError_t err = hipSuccess;
-  // The caller's event, re-recorded: a stream wait takes the record current
-  // when the wait is enqueued.  sb first waits for everything already queued
-  // on sa.
-  hipEvent_t ev = (hipEvent_t)event;
-  if (pipelined) {
-    if ((err = hipEventRecord(ev, sa)) == hipSuccess) err = hipStreamWaitEvent(sb, ev, 0);
-  }
-  if (!pipelined) {
-    err = ei::launch_probe(q, k, ps_all, probe_scale, log_scores, entropy, workspace, sa);
-    if (err == hipSuccess)
-      err = ei::launch_select(log_scores, entropy, ss_all, head_is_rigid, budget_blocks,
-                              block_idx, block_cnt, sa);
-    if (err == hipSuccess)
-      err = ei::launch_attention(q, k, v, as_all, ei::kSparse, block_idx, block_cnt, o, sa);
-    return from_hip(err);
-  }
-  for (int64_t grp = 0; grp < n_groups && err == hipSuccess; ++grp) {
-    const int64_t h0 = grp * G;   // first query head of the group, over (batch, head)
-    const uint16_t* qg = q + (size_t)h0 * qkv;
-    const uint16_t* kg = k + (size_t)grp * qkv;
-    const uint16_t* vg = v + (size_t)grp * qkv;
-    float* lsg = log_scores + (size_t)h0 * z.CS * z.CB;
-    float* eng = entropy + (size_t)h0 * z.CS;
-    err = ei::launch_probe(qg, kg, ps, probe_scale, lsg, eng, workspace, sa);
-    if (err == hipSuccess) err = hipEventRecord(ev, sa);
-    if (err == hipSuccess) err = hipStreamWaitEvent(sb, ev, 0);
-    if (err == hipSuccess)
-      err = ei::launch_select(lsg, eng, ss, head_is_rigid + h0, budget_blocks + h0 * z.CS,
-                              block_idx + (size_t)h0 * z.CS * kmax, block_cnt + h0 * z.CS, sb);
-    if (err == hipSuccess)
-      err = ei::launch_attention(qg, kg, vg, as, ei::kSparse, block_idx + (size_t)h0 * z.CS * kmax,
-                                 block_cnt + h0 * z.CS, o + (size_t)h0 * qkv, sb);
-  }
-  // sa waits for the last work on sb
-  if (err == hipSuccess) err = hipEventRecord(ev, sb);
-  if (err == hipSuccess) err = hipStreamWaitEvent(sa, ev, 0);
+  if (!workspace || workspace_bytes < ei::probe_workspace_bytes(ps)) return EI_ERR_WORKSPACE;
+  if (!aligned16({workspace})) return EI_ERR_UNSUPPORTED;
+  const ei::AttnShape as{(int)z.B, (int)z.Hq, (int)z.Hkv, (int)z.N, tiling.seg_len,
+                         tiling.block_len, (int)z.CS, (int)z.CB, kmax, softmax_scale};
+  // The three stages over the whole layer, in order on one stream.  (Running
+  // the probe of one KV group beside the attention of the previous one
+  // measured slower: both are bound by vector ALU work, and eight per-group
+  // attention launches add their tails.)
+  hipStream_t s0 = (hipStream_t)stream;
+  hipError_t err = ei::launch_probe(q, k, ps, probe_scale, log_scores, entropy, workspace, s0);
+  if (err == hipSuccess)
+    err = ei::launch_select(log_scores, entropy, ss, head_is_rigid, budget_blocks, block_idx,
+                            block_cnt, s0);
+  if (err == hipSuccess)
+    err = ei::launch_attention(q, k, v, as, ei::kSparse, block_idx, block_cnt, o, s0);
   return from_hip(err);
 }
 

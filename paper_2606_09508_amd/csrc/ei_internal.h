@@ -112,12 +112,10 @@ struct ProbeShape {
   int B, Hq, Hkv, N, Ls, Lb, CS, CB, r;
 };
 
-// Workspace layout of the probe: Q representation (binary64) then K
-// representation (fp32, blocks padded to a multiple of 64), both 256-byte
-// aligned.
-size_t probe_qrep_bytes(const ProbeShape& s);
-size_t probe_krep_bytes(const ProbeShape& s);
-// Largest C_B the scores kernel supports (LDS bound); 0 if none.
+// Workspace of the probe: the pooled query and key vectors' limb records,
+// residual parts and scales (layout in ei_probe.hip), 256-byte aligned parts.
+size_t probe_workspace_bytes(const ProbeShape& s);
+// Whether the probe kernels support the shape (every validated shape).
 bool probe_supported(const ProbeShape& s);
 
 hipError_t launch_probe(const uint16_t* q, const uint16_t* k, const ProbeShape& s,

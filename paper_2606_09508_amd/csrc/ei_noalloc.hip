@@ -43,15 +43,13 @@ extern "C" ei_status ei_entropy_guided_prefill_noalloc(
     const uint16_t* q, const uint16_t* k, const uint16_t* v, ei_dims dims, ei_tiling tiling,
     double probe_scale, ei_budget_params params, int32_t mode, int32_t kmax, float softmax_scale,
     float* log_scores, float* entropy, uint8_t* head_is_rigid, int32_t* budget_blocks,
-    int32_t* block_idx, int32_t* block_cnt, uint16_t* o, void* stream, void* stream_aux,
-    void* event) {
+    int32_t* block_idx, int32_t* block_cnt, uint16_t* o, void* stream) {
   // Every argument check of the workspace entry point first, without a
   // workspace: a valid, non-empty problem then stops at the workspace check
   // (the last one) and nothing has been launched or looked up.
   ei_status st = ei_entropy_guided_prefill(
       q, k, v, dims, tiling, probe_scale, params, mode, kmax, softmax_scale, log_scores, entropy,
-      head_is_rigid, budget_blocks, block_idx, block_cnt, o, nullptr, 0, stream, stream_aux,
-      event);
+      head_is_rigid, budget_blocks, block_idx, block_cnt, o, nullptr, 0, stream);
   if (st != EI_ERR_WORKSPACE) return st;
   if (ei_prefill_workspace_bytes(dims, tiling) > kScratchBytes) return EI_ERR_WORKSPACE;
   void* ws = scratch_address();
@@ -59,5 +57,5 @@ extern "C" ei_status ei_entropy_guided_prefill_noalloc(
   return ei_entropy_guided_prefill(q, k, v, dims, tiling, probe_scale, params, mode, kmax,
                                    softmax_scale, log_scores, entropy, head_is_rigid,
                                    budget_blocks, block_idx, block_cnt, o, ws, kScratchBytes,
-                                   stream, stream_aux, event);
+                                   stream);
 }

@@ -2,81 +2,235 @@
 // (observation attention from the four max/min logit products) and the row
 // entropy of Section 4.2, for every (batch, query head, segment).
 //
+// Exact logits on int8 MFMA.  Every pooled element is a bf16 value.  A pooled
+// vector x (128 elements) is written as x = 2^F n + x_r, with F = E - 13 for
+// E the binary exponent of max |x_i| (so |n_i| < 2^14), n_i = trunc(x_i 2^-F)
+// split into a low limb n_i & 127 (0..127) and a high limb n_i >> 7
+// (-128..127), and x_r the part below the grid 2^F (bf16-exact: it holds the
+// low bits of x_i).  Elements down to 2^-6 of the vector's maximum lie on the
+// grid.  For a query vector q and a key vector k, <q_g, k_g> with
+// q_g = 2^Fq n_q is an integer dot product of limbs: four int8 products of
+// 128 terms, each exact in int32, combined as
+//   T = P00 + 2^7 (P01 + P10) + 2^14 P11      (|T| < 2^36, exact in binary64)
+// and <q, k> = 2^(Fq + Fk) T + <q_r, k> + <q_g, k_r>.  The residual part is a
+// bf16 MFMA with fp32 accumulation; it runs only for tiles where its bound
+// sum|q_r| max|k| + max|q| sum|k_r| can exceed 2^-30 (scaled by probe_scale),
+// so a skipped residual moves a logit by less than 2^-30.  Without residuals
+// the logits equal the plain binary64 definition up to its own rounding.
+//
 // Two kernels:
-//  pool_kernel    streams Q and K once from HBM (the bound of the probe) and
-//                 writes Q_max/Q_min per segment in binary64 (so the scores
-//                 kernel can read them as uniform scalar operands) and
-//                 K_max/K_min per key block in fp32 (exact: pooled values are
-//                 input values; one convert to binary64 per use), tiled by 64
-//                 blocks: [head][j / 64][max|min][d / 4][j % 64][4], so that
-//                 the scores kernel's loads (lane = block, 4 dims per load)
-//                 read 1 KB contiguous per wave instruction.
-//  scores_kernel  one workgroup per (b, KV head, segment, chunk of query
-//                 heads).  Each lane owns one visible key block and forms the
-//                 4 logits of every query head of the chunk in binary64 FMA
-//                 (products of bf16 values are exact, so the logits equal the
-//                 plain definition's); the query representation is staged in
-//                 LDS and read with broadcast loads (in-order completion, so
-//                 they pipeline, unlike scalar loads); the kernel keeps fp32
-//                 offsets from a per-wave reference in LDS; then one wave per
-//                 logit row finds the
-//                 row's maximum, argmax and log-sum-exp, and the waves of
-//                 each head evaluate A = max((S1+S2)/2, (S3+S4)/2) and
-//                 H = -sum A ln A in log space (fp32 terms, fp64 sums).
+//  pool_kernel   streams Q and K once from HBM (the bound of the probe),
+//                pools each L_S-row query segment and L_B-row key block to
+//                its max / min vectors and writes their limbs, residual
+//                parts and scales: query records per vector, key records
+//                tiled by 16 blocks in the order the MFMA operands are read.
+//  scores_kernel one workgroup of 4 waves per (batch, KV head, 16 query
+//                units), a unit being one (query head, segment) of the KV
+//                group, segment-major.  Each wave owns 4 units as one
+//                16-row MFMA tile (rows: unit, max/min, limb) and streams
+//                over the visible key blocks 16 at a time (columns: blocks;
+//                the max and the min key vectors are two MFMAs), the key
+//                limbs staged once per workgroup in LDS.  Each lane then
+//                holds all 4 logits of one (unit, block).  Two passes: the
+//                first keeps, per lane and logit row, the running maximum,
+//                the argmax (lowest index on ties) and the sum of
+//                exp(x - max) over the other entries, merged across the 16
+//                lanes of a unit at the end; the second recomputes the
+//                logits and writes ln A = ln max((S1+S2)/2, (S3+S4)/2) and
+//                accumulates -sum A ln A.  At the entry that is the argmax of
+//                both softmaxes of a pair, ln((S_a + S_b)/2) is taken as
+//                log1p(-(d_a + d_b)/2) with d = 1 - S[argmax] = rest/(1+rest),
+//                which keeps the tiny entropies of near one-hot rows exact.
 #include "ei_internal.h"
 
 #include <math.h>
 
+// Both passes must form bitwise the same logits (the argmax's offset from the
+// row maximum is then exactly 0): no implicit FMA contraction.
+#pragma clang fp contract(off)
+
 namespace ei {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kWavesPerBlock = kThreads / kWave;
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-// K representation tile: 64 blocks x (max, min) x 128 dims in fp32.
-constexpr int kKTileBlocks = 64;
-constexpr int kKTileFloats = kKTileBlocks * 2 * kHeadDim;
-__host__ __device__ inline int padded_blocks(int CB) {
-  return (CB + kKTileBlocks - 1) / kKTileBlocks * kKTileBlocks;
-}
-// Offset (floats) of block j's value for dims 4 dq .. 4 dq + 3 of part m
-// (0 = max, 1 = min) inside one head's K representation.
-__host__ __device__ inline size_t krep_offset(int j, int m, int dq) {
-  return (size_t)(j / kKTileBlocks) * kKTileFloats +
-         (size_t)((m * (kHeadDim / 4) + dq) * kKTileBlocks + j % kKTileBlocks) * 4;
+constexpr int kFracBits = 13;                 // F = E - 13, |n| < 2^14
+constexpr int kTileBlocks = 16;               // key blocks per MFMA column tile
+constexpr int kKLimbTile = 8192;              // bytes: 16 blocks x (max, min) x 2 limbs x 128
+constexpr int kKMetaTile = 1024;              // bytes: 16 blocks x (max, min) x 32
+constexpr int kKCorrTile = 16384;             // bytes: 16 blocks x (max, min) x (k, k_r) x 128 bf16
+constexpr int kQLimb = 2 * kHeadDim;          // bytes per query vector: 2 limbs
+constexpr int kQCorr = 2 * kHeadDim;          // bf16 per query vector: q_r then q_g
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.69314718055994531f;
+
+struct QMeta {
+  double scale;   // 2^Fq (NaN if the vector has a non-finite element)
+  float R;        // sum |q_r|
+  float A;        // max |q|
+};
+struct KMeta {
+  double sk;      // sign(probe_scale) 2^Fk (NaN if non-finite)
+  double sk14;    // 2^14 sk
+  float R;        // sum |k_r|
+  float A;        // max |k|
+  float pad[2];
+};
+static_assert(sizeof(QMeta) == 16 && sizeof(KMeta) == 32, "record sizes");
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Layout {   // byte offsets of the probe records inside the workspace
+  size_t qlimb, qcorr, qmeta, klimb, kmeta, kcorr, total;
+};
+Layout layout(const ProbeShape& s) {
+  const size_t nq = (size_t)s.B * s.Hq * s.CS * 2;   // query vectors
+  const size_t nkt = (size_t)s.B * s.Hkv * ((s.CB + kTileBlocks - 1) / kTileBlocks);
+  Layout L{};
+  size_t o = 0;
+  L.qlimb = o; o = align_up(o + nq * kQLimb);
+  L.qcorr = o; o = align_up(o + nq * kQCorr * 2);
+  L.qmeta = o; o = align_up(o + nq * sizeof(QMeta));
+  L.klimb = o; o = align_up(o + nkt * kKLimbTile);
+  L.kmeta = o; o = align_up(o + nkt * kKMetaTile);
+  L.kcorr = o; o = align_up(o + nkt * kKCorrTile);
+  L.total = o;
+  return L;
 }
 
-__global__ __launch_bounds__(kThreads) void pool_kernel(
+// ---------------------------------------------------------------------------
+// Pooling and the fixed-point split
+// ---------------------------------------------------------------------------
+
+constexpr int kPoolThreads = 256;
+constexpr int kPoolWaves = kPoolThreads / kWave;
+
+__device__ __forceinline__ float row16_max(float v) {
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ float row16_sum(float v) {
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ int row16_or(int v) {
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) v |= __shfl_xor(v, o);
+  return v;
+}
+
+// The split of one pooled vector, for the 8 elements (dims 8c .. 8c+7) a lane
+// of a 16-lane row holds; every lane of the row returns the vector's scale,
+// residual sum and maximum.
+struct Split {
+  uint32_t lo[2], hi[2];   // int8 limbs, 4 per word
+  uint32_t xr[4], xg[4];   // bf16 pairs: below-grid part, grid part
+  int F;
+  bool nonfinite;
+  float R, A;
+};
+
+__device__ __forceinline__ uint32_t bf16_bits(float f) { return __float_as_uint(f) >> 16; }
+
+__device__ __forceinline__ Split split_vector(const float* x) {
+  Split o;
+  float amax = 0.0f;
+  int nf = 0;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float ax = fabsf(x[e]);
+    nf |= !(ax <= 3.40282347e38f);   // inf or NaN
+    amax = fmaxf(amax, ax);
+  }
+  amax = row16_max(amax);
+  nf = row16_or(nf);
+  int ex = 0;
+  (void)frexpf(amax, &ex);            // amax = m 2^ex, m in [0.5, 1)
+  const int F = amax > 0.0f ? ex - 1 - kFracBits : 0;
+  float R = 0.0f;
+#pragma unroll
+  for (int w = 0; w < 2; ++w) { o.lo[w] = 0u; o.hi[w] = 0u; }
+#pragma unroll
+  for (int e = 0; e < 8; e += 2) {
+    float g2[2], r2[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const float v = nf ? 0.0f : x[e + u];
+      const int n = (int)truncf(ldexpf(v, -F));          // exact: |v 2^-F| < 2^14
+      const float g = ldexpf((float)n, F);                // exact
+      const float rr = v - g;                             // exact, bf16-representable
+      R += fabsf(rr);
+      g2[u] = g;
+      r2[u] = rr;
+      const int sh = 8 * ((e + u) & 3);
+      o.lo[(e + u) >> 2] |= (uint32_t)(n & 127) << sh;
+      o.hi[(e + u) >> 2] |= (uint32_t)((n >> 7) & 255) << sh;
+    }
+    o.xg[e >> 1] = bf16_bits(g2[0]) | (bf16_bits(g2[1]) << 16);
+    o.xr[e >> 1] = bf16_bits(r2[0]) | (bf16_bits(r2[1]) << 16);
+  }
+  o.R = nf ? 0.0f : row16_sum(R);
+  o.A = nf ? 0.0f : amax;
+  o.F = F;
+  o.nonfinite = nf != 0;
+  return o;
+}
+
+// One wave per item: a query segment (B*Hq*C_S items) or a key block slot
+// (B*Hkv*C_Bt*16 items, C_Bt = ceil(C_B / 16); slots past C_B are written as
+// zeros).  Lanes c = lane % 16 hold dims 8c .. 8c+7 of rows of phase
+// lane / 16; after the reduction lanes 0-15 split the max vector and lanes
+// 16-31 the min vector.
+__global__ __launch_bounds__(kPoolThreads) void pool_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, int B, int Hq, int Hkv,
-    int N, int Ls, int Lb, int CS, int CB, double* __restrict__ qrep,
-    float* __restrict__ krep) {
+    int N, int Ls, int Lb, int CS, int CB, int CBt, double sgn, unsigned char* __restrict__ ws,
+    Layout lay) {
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t item = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
-  const int64_t nq = (int64_t)B * Hq * CS, nk = (int64_t)B * Hkv * CB;
+  const int64_t item = (int64_t)blockIdx.x * kPoolWaves + (threadIdx.x >> 6);
+  const int64_t nq = (int64_t)B * Hq * CS, nk = (int64_t)B * Hkv * CBt * kTileBlocks;
   if (item >= nq + nk) return;
   const bool is_q = item < nq;
-  const int64_t head = is_q ? item / CS : (item - nq) / CB;
-  const int grp = (int)(is_q ? item % CS : (item - nq) % CB);
-  const int L = is_q ? Ls : Lb;
-  const int64_t row0 = (int64_t)grp * L;
-  const int rows = (int)min((int64_t)L, (int64_t)N - row0);
-  const uint16_t* base = (is_q ? q : k) + ((size_t)head * N + row0) * kHeadDim;
-
+  const int64_t head = is_q ? item / CS : (item - nq) / ((int64_t)CBt * kTileBlocks);
+  const int grp = (int)(is_q ? item % CS : (item - nq) % ((int64_t)CBt * kTileBlocks));
   const int c = lane & 15;   // 16-byte chunk: dims 8c .. 8c+7
   const int ph = lane >> 4;  // row phase 0..3
+
   float mx[8], mn[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) { mx[e] = -INFINITY; mn[e] = INFINITY; }
-
-  int r = ph;
-  for (; r + 12 < rows; r += 16) {
-    uint4 w[4];
+  const bool pad = !is_q && grp >= CB;
+  if (!pad) {
+    const int L = is_q ? Ls : Lb;
+    const int64_t row0 = (int64_t)grp * L;
+    const int rows = (int)min((int64_t)L, (int64_t)N - row0);
+    const uint16_t* base = (is_q ? q : k) + ((size_t)head * N + row0) * kHeadDim;
+    int r = ph;
+    for (; r + 12 < rows; r += 16) {
+      uint4 w[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-      w[u] = *(const uint4*)(base + (size_t)(r + 4 * u) * kHeadDim + 8 * c);
+      for (int u = 0; u < 4; ++u)
+        w[u] = *(const uint4*)(base + (size_t)(r + 4 * u) * kHeadDim + 8 * c);
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const uint32_t ww[4] = {w[u].x, w[u].y, w[u].z, w[u].w};
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t ww[4] = {w[u].x, w[u].y, w[u].z, w[u].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float lo = bf16_lo(ww[e]), hi = bf16_hi(ww[e]);
+          mx[2 * e] = fmaxf(mx[2 * e], lo);
+          mn[2 * e] = fminf(mn[2 * e], lo);
+          mx[2 * e + 1] = fmaxf(mx[2 * e + 1], hi);
+          mn[2 * e + 1] = fminf(mn[2 * e + 1], hi);
+        }
+      }
+    }
+    for (; r < rows; r += 4) {
+      const uint4 w = *(const uint4*)(base + (size_t)r * kHeadDim + 8 * c);
+      const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const float lo = bf16_lo(ww[e]), hi = bf16_hi(ww[e]);
@@ -86,347 +240,433 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(
         mn[2 * e + 1] = fminf(mn[2 * e + 1], hi);
       }
     }
-  }
-  for (; r < rows; r += 4) {
-    const uint4 w = *(const uint4*)(base + (size_t)r * kHeadDim + 8 * c);
-    const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float lo = bf16_lo(ww[e]), hi = bf16_hi(ww[e]);
-      mx[2 * e] = fmaxf(mx[2 * e], lo);
-      mn[2 * e] = fminf(mn[2 * e], lo);
-      mx[2 * e + 1] = fmaxf(mx[2 * e + 1], hi);
-      mn[2 * e + 1] = fminf(mn[2 * e + 1], hi);
-    }
-  }
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    mx[e] = fmaxf(mx[e], __shfl_xor(mx[e], 16));
-    mx[e] = fmaxf(mx[e], __shfl_xor(mx[e], 32));
-    mn[e] = fminf(mn[e], __shfl_xor(mn[e], 16));
-    mn[e] = fminf(mn[e], __shfl_xor(mn[e], 32));
-  }
-  if (ph != 0) return;
-  if (is_q) {
-    double* out = qrep + ((size_t)head * CS + grp) * 2 * kHeadDim + 8 * c;
-#pragma unroll
-    for (int e = 0; e < 8; e += 2) {
-      *(double2*)(out + e) = make_double2((double)mx[e], (double)mx[e + 1]);
-      *(double2*)(out + kHeadDim + e) = make_double2((double)mn[e], (double)mn[e + 1]);
+    for (int e = 0; e < 8; ++e) {
+      mx[e] = fmaxf(mx[e], __shfl_xor(mx[e], 16));
+      mx[e] = fmaxf(mx[e], __shfl_xor(mx[e], 32));
+      mn[e] = fminf(mn[e], __shfl_xor(mn[e], 16));
+      mn[e] = fminf(mn[e], __shfl_xor(mn[e], 32));
     }
   } else {
-    float* out = krep + (size_t)head * padded_blocks(CB) * 2 * kHeadDim;
-    *(float4*)(out + krep_offset(grp, 0, 2 * c)) = make_float4(mx[0], mx[1], mx[2], mx[3]);
-    *(float4*)(out + krep_offset(grp, 0, 2 * c + 1)) = make_float4(mx[4], mx[5], mx[6], mx[7]);
-    *(float4*)(out + krep_offset(grp, 1, 2 * c)) = make_float4(mn[0], mn[1], mn[2], mn[3]);
-    *(float4*)(out + krep_offset(grp, 1, 2 * c + 1)) = make_float4(mn[4], mn[5], mn[6], mn[7]);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) { mx[e] = 0.0f; mn[e] = 0.0f; }
+  }
+  if (ph >= 2) return;
+  const int m = ph;   // 0: max vector, 1: min vector
+  const Split sp = split_vector(m == 0 ? mx : mn);
+  const uint2 lo = make_uint2(sp.lo[0], sp.lo[1]), hi = make_uint2(sp.hi[0], sp.hi[1]);
+  const uint4 xr = make_uint4(sp.xr[0], sp.xr[1], sp.xr[2], sp.xr[3]);
+  const uint4 xg = make_uint4(sp.xg[0], sp.xg[1], sp.xg[2], sp.xg[3]);
+  if (is_q) {
+    const size_t v = (size_t)item * 2 + m;   // query vector index
+    unsigned char* ql = ws + lay.qlimb + v * kQLimb;
+    *(uint2*)(ql + 8 * c) = lo;
+    *(uint2*)(ql + kHeadDim + 8 * c) = hi;
+    uint16_t* qc = (uint16_t*)(ws + lay.qcorr) + v * kQCorr;
+    *(uint4*)(qc + 8 * c) = xr;
+    *(uint4*)(qc + kHeadDim + 8 * c) = xg;
+    if (c == 0)
+      ((QMeta*)(ws + lay.qmeta))[v] =
+          QMeta{sp.nonfinite ? (double)NAN : ldexp(1.0, sp.F), sp.R, sp.A};
+  } else {
+    const int t = grp / kTileBlocks, j = grp % kTileBlocks;
+    const size_t tile = (size_t)head * CBt + t;
+    // limb l of dims d = 8c .. 8c+7: sub-block ((m, l), d / 64), then lane
+    // ((d % 64) / 16) * 16 + j, byte (d % 16)
+    unsigned char* kl = ws + lay.klimb + tile * kKLimbTile;
+    const int ks = c >> 3, cc = (c & 7) >> 1, e0 = 8 * (c & 1);
+    *(uint2*)(kl + ((m * 2 + 0) * 2 + ks) * 1024 + (cc * 16 + j) * 16 + e0) = lo;
+    *(uint2*)(kl + ((m * 2 + 1) * 2 + ks) * 1024 + (cc * 16 + j) * 16 + e0) = hi;
+    // [k | k_r] as 256 bf16 of one MFMA operand column: element 128 p + d at
+    // sub-block (128 p + d) / 32, lane ((d % 32) / 8) * 16 + j
+    unsigned char* kc = ws + lay.kcorr + tile * kKCorrTile + m * (kKCorrTile / 2);
+    uint4 korig;
+    {
+      const float* xv = m == 0 ? mx : mn;
+      korig = make_uint4(bf16_bits(xv[0]) | (bf16_bits(xv[1]) << 16),
+                         bf16_bits(xv[2]) | (bf16_bits(xv[3]) << 16),
+                         bf16_bits(xv[4]) | (bf16_bits(xv[5]) << 16),
+                         bf16_bits(xv[6]) | (bf16_bits(xv[7]) << 16));
+      if (sp.nonfinite) korig = make_uint4(0, 0, 0, 0);
+    }
+    *(uint4*)(kc + (c >> 2) * 1024 + ((c & 3) * 16 + j) * 16) = korig;
+    *(uint4*)(kc + (4 + (c >> 2)) * 1024 + ((c & 3) * 16 + j) * 16) = xr;
+    if (c == 0) {
+      const double sk = sp.nonfinite ? (double)NAN : sgn * ldexp(1.0, sp.F);
+      ((KMeta*)(ws + lay.kmeta + tile * kKMetaTile))[m * kTileBlocks + j] =
+          KMeta{sk, sk * 16384.0, sp.R, sp.A, {0.0f, 0.0f}};
+    }
   }
 }
 
-__device__ __forceinline__ void widen4(const float4 w, double* out) {
-  out[0] = (double)w.x;
-  out[1] = (double)w.y;
-  out[2] = (double)w.z;
-  out[3] = (double)w.w;
+// ---------------------------------------------------------------------------
+// Logits, softmax statistics, ln A and the entropy
+// ---------------------------------------------------------------------------
+
+constexpr int kThreads = 256;                       // 4 waves
+// One row tile (4 units) per wave, 16 units per workgroup.  Two row tiles
+// per wave share each staged key tile over twice the rows but need ~190
+// VGPRs (2 waves per SIMD against 4): 5% slower on the 128k layer.
+constexpr int KT = 1;
+constexpr int kUnits = kThreads / kWave * 4 * KT;
+constexpr int kStageBytes = kKLimbTile + kKMetaTile;
+
+__device__ __forceinline__ float hw_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float hw_log2(float x) { return __builtin_amdgcn_logf(x); }
+
+// log2((2^u + 2^v) / 2) for u, v <= 0.
+__device__ __forceinline__ float log2_pair_avg(float u, float v) {
+  const float hi = fmaxf(u, v), lo = fminf(u, v);
+  return hi + (hw_log2(1.0f + hw_exp2(lo - hi)) - 1.0f);
 }
 
-constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kLn2 = 0.69314718055994531f;
-
-// e^x and ln(1 + y) for y in [0, 1] on the hardware exp2 / log2 (relative
-// error ~1e-7 for the arguments used here; the one entry per row that needs
-// ln of a value near 1 is evaluated in binary64 instead).
-__device__ __forceinline__ float fast_exp(float x) { return __builtin_amdgcn_exp2f(x * kLog2e); }
-__device__ __forceinline__ float fast_log1p01(float y) { return __builtin_amdgcn_logf(1.0f + y) * kLn2; }
-
-// ln((exp(a) + exp(b)) / 2) for a, b <= 0, not both near 0.
-__device__ __forceinline__ float log_pair_avg(float a, float b) {
-  const float hi = fmaxf(a, b), lo = fminf(a, b);
-  return hi + fast_log1p01(fast_exp(lo - hi)) - kLn2;
+__device__ __forceinline__ double shfl_xor_f64(double v, int o) {
+  const int2 w = __builtin_bit_cast(int2, v);
+  return __builtin_bit_cast(double, make_int2(__shfl_xor(w.x, o), __shfl_xor(w.y, o)));
 }
 
-// Per-row statistics of the four softmaxes, kept in LDS between phases.
-struct RowStats {
-  float M;       // max of the per-wave references
-  float best;    // largest offset (the argmax's)
-  int bj;        // argmax (lowest index among equal offsets)
-  float lse;     // log1p(rest), rest = sum over j != argmax of exp(x_j - x_argmax)
-  double dfc;    // 1 - S[argmax] = rest / (1 + rest)
-};
+// Binary64 logit (in units of 2^Fq |probe_scale|, sign folded into sk) of
+// query vector a of the lane's unit against key vector bk of the lane's
+// block, from the limb products acc[bk][beta][2 a + alpha].
+__device__ __forceinline__ double limb_logit(const i32x4 (&acc)[2][2], int a, int bk,
+                                             double sk, double sk14) {
+  const int p00 = acc[bk][0][2 * a], p01 = acc[bk][1][2 * a];
+  const int p10 = acc[bk][0][2 * a + 1], p11 = acc[bk][1][2 * a + 1];
+  const int x = p00 + (p01 + p10) * 128;   // |x| < 2^30
+  return fma((double)p11, sk14, (double)x * sk);
+}
 
-// HPW query heads per workgroup of NT threads; rows of the score block: the 4
-// logit products (S1..S4) of each head.
-template <int HPW, int NT>
-__global__ __launch_bounds__(NT) void scores_kernel(
-    const double* __restrict__ qrep, const float* __restrict__ krep,
-    float* __restrict__ log_scores, float* __restrict__ entropy, int Hq, int Hkv, int CS,
-    int CB, int r, int s_lo, int s_hi, int n_hc, int ldy, double probe_scale) {
-  constexpr int R = 4 * HPW;
-  constexpr int W = NT / kWave;
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
-  RowStats* stats = (RowStats*)smem_raw;                        // [R]
-  double* hpart = (double*)(smem_raw + sizeof(RowStats) * R);   // [W]
-  double* qs = hpart + W;                                       // [HPW][128][max, min]
-  float* ys = (float*)(qs + HPW * 2 * kHeadDim);                // [R][ldy] offsets x - ref
-  float* refs = ys + R * ldy;                                   // [R][ldy / 64] references
-  const int nref = ldy >> 6;
-
-  int64_t id = blockIdx.x;
-  const int ns = s_hi - s_lo;
-  const int s = s_hi - 1 - (int)(id % ns);   // heavier segments first
-  id /= ns;
-  const int hc = (int)(id % n_hc);
-  id /= n_hc;
-  const int g = (int)(id % Hkv);
-  const int b = (int)(id / Hkv);
+__global__ __launch_bounds__(kThreads, 4) void scores_kernel(
+    const unsigned char* __restrict__ ws, Layout lay, float* __restrict__ log_scores,
+    float* __restrict__ entropy, int Hq, int Hkv, int CS, int CB, int CBt, int r, int n_groups,
+    int n_chunks, double ps_abs, double sgn, float tau) {
+  __shared__ __attribute__((aligned(16))) unsigned char stage[2][kStageBytes];
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int gq = lane >> 4, col = lane & 15;
+  const int wg = blockIdx.x;
+  const int chunk = n_chunks - 1 - wg / n_groups;   // heavier chunks first
+  const int gi = wg % n_groups;                      // (batch, KV head)
+  const int b = gi / Hkv, g = gi % Hkv;
   const int G = Hq / Hkv;
-  const int h0 = g * G + hc * HPW;
-  const int nh = min(HPW, G - hc * HPW);
-  const int nvis = min((s + 1) * r, CB);
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
+  const int U = G * CS;
+  const int u0 = chunk * kUnits;
+  const int ulast = min(u0 + kUnits - 1, U - 1);
+  const int nv_max = min((ulast / G + 1) * r, CB);
+  const int nt = (nv_max + kTileBlocks - 1) / kTileBlocks;
 
-  for (int t = threadIdx.x; t < HPW * 2 * kHeadDim; t += NT) {
-    const int hh = t / (2 * kHeadDim), m = (t / kHeadDim) & 1, d = t % kHeadDim;
-    const double* qv = qrep + ((size_t)(b * Hq + h0 + min(hh, nh - 1)) * CS + s) * 2 * kHeadDim;
-    qs[(hh * kHeadDim + d) * 2 + m] = qv[m * kHeadDim + d];
+  const QMeta* qmeta = (const QMeta*)(ws + lay.qmeta);
+  const unsigned char* qlimb = ws + lay.qlimb;
+  const uint16_t* qcorr = (const uint16_t*)(ws + lay.qcorr);
+  const unsigned char* klimb = ws + lay.klimb + (size_t)gi * CBt * kKLimbTile;
+  const unsigned char* kmeta = ws + lay.kmeta + (size_t)gi * CBt * kKMetaTile;
+  const unsigned char* kcorr = ws + lay.kcorr + (size_t)gi * CBt * kKCorrTile;
+
+  auto unit_row = [&](int u) -> int64_t {   // (b, h, s) row of unit u
+    const int s = u / G, hh = u % G;
+    return ((int64_t)(b * Hq + g * G + hh)) * CS + s;
+  };
+
+  // This lane's units (D rows 4 gq .. 4 gq + 3 of each tile): row, visible
+  // blocks (0 for a unit past the group's last), per query vector a the
+  // log2-unit scale c2 and the residual factor iq = sign / 2^Fq.
+  int64_t urow[KT];
+  int nv[KT];
+  float c2[KT][2];
+  double iq[KT][2];
+  float Aqm[KT], Rqm[KT];
+  // A operands: row i = col holds (unit i / 4, vector (i >> 1) & 1, limb i & 1)
+  i32x4 aop[KT][2];
+#pragma unroll
+  for (int kt = 0; kt < KT; ++kt) {
+    const int u = u0 + 4 * KT * wave + 4 * kt + gq;
+    const bool uv = u < U;
+    urow[kt] = uv ? unit_row(u) : 0;
+    nv[kt] = uv ? min((u / G + 1) * r, CB) : 0;
+    float am = 0.0f, rm = 0.0f;
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      const QMeta qm = uv ? qmeta[urow[kt] * 2 + a] : QMeta{1.0, 0.0f, 0.0f};
+      c2[kt][a] = ps_abs == 0.0 ? 1.0f : (float)(ps_abs * qm.scale * (double)kLog2e);
+      iq[kt][a] = sgn / qm.scale;
+      am = fmaxf(am, qm.A);
+      rm = fmaxf(rm, qm.R);
+    }
+    am = fmaxf(am, __shfl_xor(am, 16));
+    am = fmaxf(am, __shfl_xor(am, 32));
+    rm = fmaxf(rm, __shfl_xor(rm, 16));
+    rm = fmaxf(rm, __shfl_xor(rm, 32));
+    Aqm[kt] = am;
+    Rqm[kt] = rm;
+    const int ui = u0 + 4 * KT * wave + 4 * kt + (col >> 2);
+    const int a = (col >> 1) & 1, al = col & 1;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      aop[kt][ks] = i32x4{0, 0, 0, 0};
+      if (ui < U)
+        aop[kt][ks] = *(const i32x4*)(qlimb + (size_t)(unit_row(ui) * 2 + a) * kQLimb +
+                                      al * kHeadDim + 64 * ks + 16 * gq);
+    }
   }
-  __syncthreads();
-  const float* kb = krep + (size_t)(b * Hkv + g) * padded_blocks(CB) * 2 * kHeadDim;
 
-  // Phase 1: exact logits, one key block per lane.
-  for (int j0 = wave * kWave; j0 < nvis; j0 += NT) {
-    const int j = j0 + lane;
-    const bool valid = j < nvis;
-    const float* kr = kb + krep_offset(valid ? j : nvis - 1, 0, 0);
-    double acc[HPW][4];
+  // The residual part of the 16 logits per row of tile kt and key tile t, if
+  // its bound can reach tau: bf16 MFMA with rows (unit, vector, 0 / pad) and
+  // the operand [q_r | q_g] . [k | k_r].  corr[bk][2 a] is the lane's value.
+  auto residual = [&](int kt, int t, f32x4 (&corr)[2]) {
+    corr[0] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    corr[1] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    const int ui = u0 + 4 * KT * wave + 4 * kt + (col >> 2);
+    const int a = (col >> 1) & 1;
+    const bool has = ui < U && (col & 1) == 0;
+    const uint16_t* qc = qcorr + (has ? (size_t)(unit_row(ui) * 2 + a) * kQCorr : 0);
+    // the tile's base is wave-uniform: only 32-bit lane offsets in vector registers
+    const unsigned char* kc =
+        kcorr + (size_t)__builtin_amdgcn_readfirstlane(t) * kKCorrTile;
 #pragma unroll
-    for (int hh = 0; hh < HPW; ++hh)
+    for (int kk = 0; kk < 8; ++kk) {
+      const uint4 qa = has ? *(const uint4*)(qc + 32 * kk + 8 * gq) : make_uint4(0, 0, 0, 0);
 #pragma unroll
-      for (int cc = 0; cc < 4; ++cc) acc[hh][cc] = 0.0;
-#pragma unroll 2
-    for (int d0 = 0; d0 < kHeadDim; d0 += 8) {
-      double kx[8], kn[8];
-      constexpr int kDq = 4 * kKTileBlocks;             // floats between dim quads
-      constexpr int kMin = (kHeadDim / 4) * kDq;        // max part -> min part
-      widen4(*(const float4*)(kr + (d0 / 4) * kDq), kx);
-      widen4(*(const float4*)(kr + (d0 / 4 + 1) * kDq), kx + 4);
-      widen4(*(const float4*)(kr + kMin + (d0 / 4) * kDq), kn);
-      widen4(*(const float4*)(kr + kMin + (d0 / 4 + 1) * kDq), kn + 4);
+      for (int bk = 0; bk < 2; ++bk) {
+        const uint32_t off = (uint32_t)(bk * (kKCorrTile / 2) + kk * 1024) + (uint32_t)lane * 16u;
+        const uint4 kb = *(const uint4*)(kc + off);
+        corr[bk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, qa),
+                                                          __builtin_bit_cast(bf16x8, kb),
+                                                          corr[bk], 0, 0, 0);
+      }
+    }
+  };
+
+  // Per tile: the staged key limbs and records, then for each row tile the
+  // eight limb MFMAs and the lane's four logits.
+  auto tile_logits = [&](const unsigned char* st, int t, int kt, double (&x)[2][2]) {
+    i32x4 acc[2][2];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
+    for (int bk = 0; bk < 2; ++bk)
 #pragma unroll
-        for (int hh = 0; hh < HPW; ++hh) {
-          const double2 qq = *(const double2*)(qs + (hh * kHeadDim + d0 + e) * 2);
-          const double qa = qq.x, qb = qq.y;
-          acc[hh][0] = fma(qa, kx[e], acc[hh][0]);   // S1: Q_max . K_max
-          acc[hh][1] = fma(qa, kn[e], acc[hh][1]);   // S2: Q_max . K_min
-          acc[hh][2] = fma(qb, kx[e], acc[hh][2]);   // S3: Q_min . K_max
-          acc[hh][3] = fma(qb, kn[e], acc[hh][3]);   // S4: Q_min . K_min
+      for (int be = 0; be < 2; ++be) {
+        acc[bk][be] = i32x4{0, 0, 0, 0};
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          const i32x4 bo = *(const i32x4*)(st + ((bk * 2 + be) * 2 + ks) * 1024 + lane * 16);
+          acc[bk][be] =
+              __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[kt][ks], bo, acc[bk][be], 0, 0, 0);
         }
       }
+    const KMeta* km = (const KMeta*)(st + kKLimbTile);
+    const KMeta k0 = km[col], k1 = km[kTileBlocks + col];
+    const bool need = fmaf(k0.R, Aqm[kt], k0.A * Rqm[kt]) > tau ||
+                      fmaf(k1.R, Aqm[kt], k1.A * Rqm[kt]) > tau;
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      x[a][0] = limb_logit(acc, a, 0, k0.sk, k0.sk14);
+      x[a][1] = limb_logit(acc, a, 1, k1.sk, k1.sk14);
     }
+    if (__builtin_amdgcn_ballot_w64(need) != 0) {
+      f32x4 corr[2];
+      residual(kt, t, corr);
 #pragma unroll
-    for (int hh = 0; hh < HPW; ++hh) {
+      for (int a = 0; a < 2; ++a)
 #pragma unroll
-      for (int cc = 0; cc < 4; ++cc) {
-        const int row = hh * 4 + cc;
-        const double x = probe_scale * acc[hh][cc];
-        const float ref = wave_max_f32_dpp(valid ? (float)x : -INFINITY);
-        if (valid) ys[row * ldy + j] = (float)(x - (double)ref);
-        if (lane == 0) refs[row * nref + (j0 >> 6)] = ref;
+        for (int bk = 0; bk < 2; ++bk) x[a][bk] = fma((double)corr[bk][2 * a], iq[kt][a], x[a][bk]);
+    }
+  };
+
+  // key tile staging: two LDS buffers, the next tile held in registers
+  uint4 p0, p1, pm;
+  auto load_tile = [&](int t) {
+    const uint4* src = (const uint4*)(klimb + (size_t)t * kKLimbTile);
+    p0 = src[tid];
+    p1 = src[kThreads + tid];
+    if (tid < kKMetaTile / 16) pm = ((const uint4*)(kmeta + (size_t)t * kKMetaTile))[tid];
+  };
+  auto store_tile = [&](int buf) {
+    uint4* dst = (uint4*)stage[buf];
+    dst[tid] = p0;
+    dst[kThreads + tid] = p1;
+    if (tid < kKMetaTile / 16) dst[kKLimbTile / 16 + tid] = pm;
+  };
+
+  // pass 1 state per row tile, query vector a and key vector bk
+  double m_[KT][2][2];
+  float rest_[KT][2][2];
+  int bj_[KT][2][2];
+#pragma unroll
+  for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int bk = 0; bk < 2; ++bk) {
+        m_[kt][a][bk] = -1.7976931348623157e308;   // a phantom entry whose weight is 0
+        rest_[kt][a][bk] = 0.0f;
+        bj_[kt][a][bk] = 0x7fffffff;
+      }
+
+  // tiles below nv_min are visible to every unit of the workgroup (when all
+  // its units exist: a unit past the group's last has no row at all)
+  const int nv_min = u0 + kUnits <= U ? min((u0 / G + 1) * r, CB) : 0;
+  load_tile(0);
+  store_tile(0);
+  if (nt > 1) load_tile(1);
+  __syncthreads();
+  for (int t = 0; t < nt; ++t) {
+    const unsigned char* st = stage[t & 1];
+    const int j = kTileBlocks * t + col;
+    const bool whole = kTileBlocks * (t + 1) <= nv_min;   // workgroup-uniform
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) {
+      double x[2][2];
+      tile_logits(st, t, kt, x);
+      if (!whole) {
+        const bool v = j < nv[kt];
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+          for (int bk = 0; bk < 2; ++bk) x[a][bk] = v ? x[a][bk] : -INFINITY;
+      }
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int bk = 0; bk < 2; ++bk) {
+          const double xv = x[a][bk];
+          double& m = m_[kt][a][bk];
+          float& rs = rest_[kt][a][bk];
+          const bool gt = xv > m;
+          const float e = hw_exp2(-fabsf((float)(xv - m)) * c2[kt][a]);
+          rs = gt ? fmaf(rs, e, e) : rs + e;
+          m = gt ? xv : m;   // a NaN logit leaves m (its weight makes rest NaN)
+          bj_[kt][a][bk] = gt ? j : bj_[kt][a][bk];
+        }
+    }
+    if (t + 1 < nt) {
+      store_tile((t + 1) & 1);
+      if (t + 2 < nt) load_tile(t + 2);
+    }
+    __syncthreads();
+  }
+
+  // merge the 16 lanes of each unit: max, lowest argmax, and the other
+  // entries' weight relative to the max
+  float lse2[KT][2][2], ltop2[KT][2];
+  int jtop[KT][2];
+#pragma unroll
+  for (int kt = 0; kt < KT; ++kt) {
+    float dfc[2][2];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int bk = 0; bk < 2; ++bk) {
+        double m = m_[kt][a][bk];
+        float rs = rest_[kt][a][bk];
+        int jj = bj_[kt][a][bk];
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) {
+          const double m2 = shfl_xor_f64(m, o);
+          const float r2 = __shfl_xor(rs, o);
+          const int j2 = __shfl_xor(jj, o);
+          const bool w1 = m > m2 || (m == m2 && jj < j2);
+          const double mw = w1 ? m : m2, ml = w1 ? m2 : m;
+          const float rw = w1 ? rs : r2, rl = w1 ? r2 : rs;
+          rs = fmaf(rl + 1.0f, hw_exp2(-(float)(mw - ml) * c2[kt][a]), rw);
+          m = mw;
+          jj = w1 ? jj : j2;
+        }
+        m_[kt][a][bk] = m;
+        bj_[kt][a][bk] = jj;
+        lse2[kt][a][bk] = log1pf(rs) * kLog2e;
+        dfc[a][bk] = rs / (1.0f + rs);
+      }
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      jtop[kt][a] = bj_[kt][a][0] == bj_[kt][a][1] ? bj_[kt][a][0] : -1;
+      ltop2[kt][a] = log1pf(-0.5f * (dfc[a][0] + dfc[a][1])) * kLog2e;
+    }
+  }
+
+  // pass 2: ln A and the entropy
+  float H2[KT];
+#pragma unroll
+  for (int kt = 0; kt < KT; ++kt) H2[kt] = 0.0f;
+  load_tile(0);
+  store_tile(0);
+  if (nt > 1) load_tile(1);
+  __syncthreads();
+  for (int t = 0; t < nt; ++t) {
+    const unsigned char* st = stage[t & 1];
+    const int j = kTileBlocks * t + col;
+    const bool whole = kTileBlocks * (t + 1) <= nv_min;   // workgroup-uniform
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) {
+      double x[2][2];
+      tile_logits(st, t, kt, x);
+      float l2[2];
+#pragma unroll
+      for (int a = 0; a < 2; ++a) {
+        float ls[2];
+#pragma unroll
+        for (int bk = 0; bk < 2; ++bk)
+          ls[bk] = fmaf((float)(x[a][bk] - m_[kt][a][bk]), c2[kt][a], -lse2[kt][a][bk]);
+        float lp = log2_pair_avg(ls[0], ls[1]);
+        asm volatile("" : "+v"(lp));   // formed for every lane, then selected
+        l2[a] = j == jtop[kt][a] ? ltop2[kt][a] : lp;
+      }
+      const float L2 = l2[0] > l2[1] ? l2[0] : l2[1];
+      const float h = hw_exp2(L2) * L2;
+      float* dst = log_scores + urow[kt] * CB + j;
+      if (whole) {
+        *dst = L2 * kLn2;
+        H2[kt] += h;
+      } else if (j < nv[kt]) {
+        *dst = L2 * kLn2;
+        H2[kt] += h;
       }
     }
-  }
-  __syncthreads();
-
-  // Phase 2a: statistics of every logit row, one wave per row.
-  const int nch = (nvis + 63) >> 6;
-  for (int row = wave; row < 4 * nh; row += W) {
-    const float* yr = ys + row * ldy;
-    const float* rr = refs + row * nref;
-    float m = -INFINITY;
-    for (int c = lane; c < nch; c += kWave) m = fmaxf(m, rr[c]);
-    const float M = wave_max_f32(m);
-    float best = -INFINITY;
-    int bj = 0x7fffffff;
-    for (int j = lane; j < nvis; j += kWave) {
-      const float dv = yr[j] + (rr[j >> 6] - M);
-      if (dv > best) { best = dv; bj = j; }
+    if (t + 1 < nt) {
+      store_tile((t + 1) & 1);
+      if (t + 2 < nt) load_tile(t + 2);
     }
+    __syncthreads();
+  }
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float ob = __shfl_xor(best, o);
-      const int oj = __shfl_xor(bj, o);
-      if (ob > best || (ob == best && oj < bj)) { best = ob; bj = oj; }
-    }
-    double rest = 0.0;
-    for (int j = lane; j < nvis; j += kWave) {
-      const float dv = yr[j] + (rr[j >> 6] - M);
-      if (j != bj) rest += (double)fast_exp(dv - best);
-    }
-    rest = wave_sum_f64(rest);
-    if (lane == 0) stats[row] = RowStats{M, best, bj, (float)log1p(rest), rest / (1.0 + rest)};
-  }
-  __syncthreads();
-
-  // Phase 2b: ln A and the entropy terms; each head's row is split over
-  // W / HPW waves.
-  constexpr int P = W / HPW;
-  const int hh = wave % HPW, part = wave / HPW;
-  double H = 0.0;
-  if (hh < nh) {
-    const int h = h0 + hh;
-    RowStats st[4];
-#pragma unroll
-    for (int cc = 0; cc < 4; ++cc) st[cc] = stats[hh * 4 + cc];
-    const float l12_top = (st[0].bj == st[1].bj) ? (float)log1p(-0.5 * (st[0].dfc + st[1].dfc)) : 0.f;
-    const float l34_top = (st[2].bj == st[3].bj) ? (float)log1p(-0.5 * (st[2].dfc + st[3].dfc)) : 0.f;
-    float* Lrow = log_scores + ((size_t)(b * Hq + h) * CS + s) * CB;
-    for (int j = part * kWave + lane; j < nvis; j += P * kWave) {
-      float ls[4];
-#pragma unroll
-      for (int cc = 0; cc < 4; ++cc) {
-        const int row = hh * 4 + cc;
-        const float dv = ys[row * ldy + j] + (refs[row * nref + (j >> 6)] - st[cc].M);
-        ls[cc] = (j == st[cc].bj) ? -st[cc].lse : (dv - st[cc].best) - st[cc].lse;
-      }
-      const float l12 = (j == st[0].bj && j == st[1].bj) ? l12_top : log_pair_avg(ls[0], ls[1]);
-      const float l34 = (j == st[2].bj && j == st[3].bj) ? l34_top : log_pair_avg(ls[2], ls[3]);
-      const float L = fmaxf(l12, l34);
-      Lrow[j] = L;
-      H -= (double)(fast_exp(L) * L);
-    }
-    H = wave_sum_f64(H);
-  }
-  if (lane == 0) hpart[wave] = H;
-  __syncthreads();
-  if ((int)threadIdx.x < nh) {
-    double Ht = 0.0;
-    for (int p = 0; p < P; ++p) Ht += hpart[p * HPW + threadIdx.x];
-    entropy[(size_t)(b * Hq + h0 + threadIdx.x) * CS + s] = (float)Ht;
-  }
-}
-
-constexpr size_t kAlign = 256;
-size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
-constexpr size_t kMaxLds = 160 * 1024;
-
-size_t scores_lds_bytes(int hpw, int nt, int ldy) {
-  const size_t R = 4 * (size_t)hpw;
-  return sizeof(RowStats) * R + sizeof(double) * (size_t)(nt / kWave) +
-         sizeof(double) * (size_t)hpw * 2 * kHeadDim + R * (size_t)ldy * 4 +
-         R * (size_t)(ldy / 64) * 4;
-}
-
-// Threads per workgroup grow with the row length so that long rows keep
-// several waves per SIMD in flight.
-int pick_threads(int ldy) { return ldy <= 512 ? 256 : (ldy <= 1024 ? 512 : 1024); }
-
-// Heads per workgroup: up to 4 query heads of one KV group share each K
-// representation load; fewer when the LDS tile for this row length would
-// not fit.  0 if even one head does not fit.
-int pick_hpw(int G, int ldy, size_t max_lds) {
-  int hpw = G >= 4 ? 4 : (G >= 2 ? 2 : 1);
-  while (hpw >= 1 && scores_lds_bytes(hpw, pick_threads(ldy), ldy) > max_lds) hpw /= 2;
-  return hpw;
-}
-
-size_t device_max_lds() {
-  int dev = 0, v = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return kMaxLds;
-  if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess ||
-      v <= 0)
-    return kMaxLds;
-  return (size_t)v < kMaxLds ? (size_t)v : kMaxLds;
-}
-
-template <int HPW, int NT>
-hipError_t launch_scores_t(const double* qrep, const float* krep, float* log_scores,
-                           float* entropy, const ProbeShape& s, int s_lo, int s_hi, int ldy,
-                           double probe_scale, hipStream_t stream) {
-  const int G = s.Hq / s.Hkv;
-  const int n_hc = (G + HPW - 1) / HPW;
-  const int64_t grid = (int64_t)s.B * s.Hkv * n_hc * (s_hi - s_lo);
-  const size_t lds = scores_lds_bytes(HPW, NT, ldy);
-  hipLaunchKernelGGL((scores_kernel<HPW, NT>), dim3((unsigned)grid), dim3(NT), lds, stream,
-                     qrep, krep, log_scores, entropy, s.Hq, s.Hkv, s.CS, s.CB, s.r, s_lo, s_hi,
-                     n_hc, ldy, probe_scale);
-  return hipGetLastError();
-}
-
-template <int HPW>
-hipError_t launch_scores_h(const double* qrep, const float* krep, float* log_scores,
-                           float* entropy, const ProbeShape& s, int s_lo, int s_hi, int ldy,
-                           double probe_scale, hipStream_t stream) {
-  switch (pick_threads(ldy)) {
-    case 256:
-      return launch_scores_t<HPW, 256>(qrep, krep, log_scores, entropy, s, s_lo, s_hi, ldy,
-                                       probe_scale, stream);
-    case 512:
-      return launch_scores_t<HPW, 512>(qrep, krep, log_scores, entropy, s, s_lo, s_hi, ldy,
-                                       probe_scale, stream);
-    default:
-      return launch_scores_t<HPW, 1024>(qrep, krep, log_scores, entropy, s, s_lo, s_hi, ldy,
-                                        probe_scale, stream);
+  for (int kt = 0; kt < KT; ++kt) {
+    const float h = row16_sum(H2[kt]);
+    if (col == 0 && nv[kt] > 0) entropy[urow[kt]] = -h * kLn2;
   }
 }
 
 }  // namespace
 
-size_t probe_qrep_bytes(const ProbeShape& s) {
-  return align_up((size_t)s.B * s.Hq * s.CS * 2 * kHeadDim * sizeof(double));
-}
-size_t probe_krep_bytes(const ProbeShape& s) {
-  return align_up((size_t)s.B * s.Hkv * padded_blocks(s.CB) * 2 * kHeadDim * sizeof(float));
-}
+size_t probe_workspace_bytes(const ProbeShape& s) { return layout(s).total; }
 
 bool probe_supported(const ProbeShape& s) {
-  const int ldy = (s.CB + 63) / 64 * 64;
-  return pick_hpw(s.Hq / s.Hkv, ldy, kMaxLds) > 0;
+  (void)s;
+  return true;
 }
 
 hipError_t launch_probe(const uint16_t* q, const uint16_t* k, const ProbeShape& s,
                         double probe_scale, float* log_scores, float* entropy, void* workspace,
                         hipStream_t stream) {
-  double* qrep = (double*)workspace;
-  float* krep = (float*)((char*)workspace + probe_qrep_bytes(s));
+  const Layout lay = layout(s);
+  unsigned char* ws = (unsigned char*)workspace;
+  const int CBt = (s.CB + kTileBlocks - 1) / kTileBlocks;
+  const double sgn = probe_scale > 0.0 ? 1.0 : (probe_scale < 0.0 ? -1.0 : 0.0);
   {
-    const int64_t items = (int64_t)s.B * s.Hq * s.CS + (int64_t)s.B * s.Hkv * s.CB;
-    const int64_t grid = (items + kWavesPerBlock - 1) / kWavesPerBlock;
-    hipLaunchKernelGGL(pool_kernel, dim3((unsigned)grid), dim3(kThreads), 0, stream, q, k, s.B,
-                       s.Hq, s.Hkv, s.N, s.Ls, s.Lb, s.CS, s.CB, qrep, krep);
+    const int64_t items = (int64_t)s.B * s.Hq * s.CS + (int64_t)s.B * s.Hkv * CBt * kTileBlocks;
+    const int64_t grid = (items + kPoolWaves - 1) / kPoolWaves;
+    hipLaunchKernelGGL(pool_kernel, dim3((unsigned)grid), dim3(kPoolThreads), 0, stream, q, k,
+                       s.B, s.Hq, s.Hkv, s.N, s.Ls, s.Lb, s.CS, s.CB, CBt, sgn, ws, lay);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  // Segments are split into launches by visible-row length so that short
-  // rows do not reserve LDS for the longest one.
   const int G = s.Hq / s.Hkv;
-  const size_t max_lds = device_max_lds();
-  int s_lo = 0;
-  while (s_lo < s.CS) {
-    const int nvis_lo = min((s_lo + 1) * s.r, s.CB);
-    int cap = 512;
-    while (cap < nvis_lo) cap *= 2;
-    // last segment whose row fits in `cap`
-    int s_hi = min(s.CS, cap / s.r);
-    if (s_hi <= s_lo) s_hi = s_lo + 1;
-    const int nvis_hi = min(s_hi * s.r, s.CB);
-    const int ldy = (nvis_hi + 63) / 64 * 64;
-    const int hpw = pick_hpw(G, ldy, max_lds);
-    hipError_t e = hipErrorInvalidValue;
-    if (hpw == 4)
-      e = launch_scores_h<4>(qrep, krep, log_scores, entropy, s, s_lo, s_hi, ldy, probe_scale,
-                             stream);
-    else if (hpw == 2)
-      e = launch_scores_h<2>(qrep, krep, log_scores, entropy, s, s_lo, s_hi, ldy, probe_scale,
-                             stream);
-    else if (hpw == 1)
-      e = launch_scores_h<1>(qrep, krep, log_scores, entropy, s, s_lo, s_hi, ldy, probe_scale,
-                             stream);
-    if (e != hipSuccess) return e;
-    s_lo = s_hi;
-  }
-  return hipSuccess;
+  const int n_groups = s.B * s.Hkv;
+  const int n_chunks = (G * s.CS + kUnits - 1) / kUnits;
+  const double ps_abs = fabs(probe_scale);
+  // skip the residual MFMA where it moves no logit by 2^-30 or more
+  const float tau = probe_scale == 0.0 ? INFINITY : (float)(0x1p-30 / ps_abs);
+  hipLaunchKernelGGL(scores_kernel, dim3((unsigned)((int64_t)n_groups * n_chunks)),
+                     dim3(kThreads), 0, stream, ws, lay, log_scores, entropy, s.Hq, s.Hkv, s.CS,
+                     s.CB, CBt, s.r, n_groups, n_chunks, ps_abs, sgn, tau);
+  return hipGetLastError();
 }
 
 }  // namespace ei

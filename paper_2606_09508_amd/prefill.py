@@ -3,8 +3,8 @@
 A Llama-3-8B-shaped decoder (random bf16 weights, no checkpoint) runs its
 prefill with the attention of every layer computed by this library: the
 entropy probe, head classification / budgets / top-k selection and the
-block-sparse kernel, in the library's one call that pipelines them over
-KV-head groups (``attn="sparse"``), or the dense causal kernel
+block-sparse kernel, in the library's one call (``attn="sparse"``), or the
+dense causal kernel
 (``attn="dense"``, the full-attention baseline).  Everything around the
 attention is the ordinary decoder layer -- RMSNorm, the Q/K/V/O projections,
 rotary position embedding, the SwiGLU MLP -- on PyTorch (the projections and

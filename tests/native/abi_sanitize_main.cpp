@@ -27,7 +27,6 @@ int main() {
   int32_t* FI = reinterpret_cast<int32_t*>(0x1000);
   uint8_t* FU = reinterpret_cast<uint8_t*>(0x1000);
   void* FV = reinterpret_cast<void*>(0x1000);
-  void* FS = reinterpret_cast<void*>(0x2000);
 
   EXPECT(ei_abi_version() > 0);
   for (int st = -7; st <= 1; ++st) EXPECT(ei_status_str((ei_status)st) != nullptr);
@@ -92,16 +91,16 @@ int main() {
     EXPECT(ei_dense_prefill_attn(F16, F16, F16, dd, 0.088f, 1, F16, nullptr) < 0);
   // the one-call path
   const size_t pws = ei_prefill_workspace_bytes(d, t);
+  EXPECT(pws == ws);
   EXPECT(ei_entropy_guided_prefill(F16, F16, F16, d, t, 1.0, p, 0, km, 0.088f, FF, FF, FU, FI,
-                                   FI, FI, F16, FV, pws, FS, nullptr, FV) == EI_ERR_SHAPE);
-  EXPECT(ei_entropy_guided_prefill(F16, F16, F16, d, t, 1.0, p, 0, km, 0.088f, FF, FF, FU, FI,
-                                   FI, FI, F16, FV, pws, FS, FS, FV) == EI_ERR_SHAPE);
-  EXPECT(ei_entropy_guided_prefill(F16, F16, F16, d, t, 1.0, p, 0, km, 0.088f, FF, FF, FU, FI,
-                                   FI, FI, F16, FV, pws - 1, FS, FV, FV) == EI_ERR_WORKSPACE);
+                                   FI, FI, F16, FV, pws - 1, nullptr) == EI_ERR_WORKSPACE);
   EXPECT(ei_entropy_guided_prefill(F16, F16, F16, d, t, 1.0, p, 7, km, 0.088f, FF, FF, FU, FI,
-                                   FI, FI, F16, FV, pws, FS, FV, FV) == EI_ERR_SHAPE);
+                                   FI, FI, F16, FV, pws, nullptr) == EI_ERR_SHAPE);
   EXPECT(ei_entropy_guided_prefill(F16, F16, nullptr, d, t, 1.0, p, 0, km, 0.088f, FF, FF, FU,
-                                   FI, FI, FI, F16, FV, pws, FS, FV, FV) == EI_ERR_NULL);
+                                   FI, FI, FI, F16, FV, pws, nullptr) == EI_ERR_NULL);
+  EXPECT(ei_entropy_guided_prefill_noalloc(F16, F16, F16, ei_dims{1, 64, 8, 262144, 128}, t,
+                                           1.0, p, 0, km, 0.088f, FF, FF, FU, FI, FI, FI, F16,
+                                           nullptr) == EI_ERR_WORKSPACE);
 
   // scales: softmax_scale finite and > 0, probe_scale finite
   for (float sc : {0.0f, -0.088f, INFINITY, -INFINITY, NAN}) {
@@ -109,15 +108,10 @@ int main() {
            EI_ERR_SHAPE);
     EXPECT(ei_dense_prefill_attn(F16, F16, F16, d, sc, 0, F16, nullptr) == EI_ERR_SHAPE);
     EXPECT(ei_entropy_guided_prefill(F16, F16, F16, d, t, 1.0, p, 0, km, sc, FF, FF, FU, FI, FI,
-                                     FI, F16, FV, pws, FS, FV, FV) == EI_ERR_SHAPE);
+                                     FI, F16, FV, pws, nullptr) == EI_ERR_SHAPE);
   }
   for (double ps : {(double)INFINITY, (double)NAN})
     EXPECT(ei_entropy_probe(F16, F16, d, t, ps, FF, FF, FV, ws, nullptr) == EI_ERR_SHAPE);
-  // the pipelined regime needs the caller's event
-  const ei_dims dl{1, 4, 1, 16384, 128};
-  EXPECT(ei_entropy_guided_prefill(F16, F16, F16, dl, t, 1.0, p, 0, km, 0.088f, FF, FF, FU, FI,
-                                   FI, FI, F16, FV, ei_prefill_workspace_bytes(dl, t), FS, FV,
-                                   nullptr) == EI_ERR_NULL);
 
   std::printf("abi sanitized run: %s\n", failures ? "FAILED" : "ok");
   return failures ? 1 : 0;

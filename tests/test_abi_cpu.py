@@ -35,7 +35,7 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_helpers(L):
-    assert L.ei_abi_version() == 4
+    assert L.ei_abi_version() == 5
     assert eb.kmax(128, 64, 2048, 3) == 98
     assert eb.kmax(2048, 64, 2048, 3) == 96 + 32
     assert eb.kmax(256, 128, 256, 3) == 6 + 2
@@ -52,8 +52,6 @@ def test_helpers(L):
 
 
 FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: every call below fails validation
-FAKE2 = ctypes.c_void_p(0x2000)  # a second fake handle (stream)
-FAKE3 = ctypes.c_void_p(0x3000)  # a fake event handle
 
 
 @pytest.mark.parametrize("dims,tiling,expect", [
@@ -125,46 +123,29 @@ def test_attention_rejects_bad_arguments(L):
     assert L.ei_dense_prefill_attn(FAKE, FAKE, FAKE, d, float("nan"), 1, FAKE, None) == -2
 
 
-def test_pipelined_prefill_rejects_bad_arguments(L):
+def test_prefill_rejects_bad_arguments(L):
     d, t = eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(128, 64)
     p = eb.budget_params(base_budget=256)
     km = L.ei_kmax(t, p)
     ws = L.ei_prefill_workspace_bytes(d, t)
-    assert ws > 0 and ws == L.ei_probe_workspace_bytes(eb.Dims(1, 4, 1, 1024, 128), t)
+    assert ws > 0 and ws == L.ei_probe_workspace_bytes(d, t)
     outs = (FAKE,) * 7
     call = L.ei_entropy_guided_prefill
     args = (FAKE, FAKE, FAKE, d, t, 1.0, p)
-    assert call(*args, 0, km, 0.088, *outs, FAKE, ws, FAKE, None, FAKE3) == -2
-    assert call(*args, 0, km, 0.088, *outs, FAKE, ws, FAKE, FAKE, FAKE3) == -2
-    assert call(*args, 5, km, 0.088, *outs, FAKE, ws, FAKE, FAKE2, FAKE3) == -2
-    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km - 1, 0.088, *outs, FAKE, ws, FAKE,
-                FAKE2, FAKE3) == -2
-    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, FAKE, ws - 1, FAKE,
-                FAKE2, FAKE3) == -4
-    assert call(None, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, FAKE, ws, FAKE,
-                FAKE2, FAKE3) == -1
+    assert call(*args, 5, km, 0.088, *outs, FAKE, ws, None) == -2
+    assert call(*args, 0, km - 1, 0.088, *outs, FAKE, ws, None) == -2
+    assert call(*args, 0, km, 0.088, *outs, FAKE, ws - 1, None) == -4
+    assert call(*args, 0, km, 0.088, *outs, None, ws, None) == -4
+    assert call(None, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, FAKE, ws, None) == -1
 
 
-def test_prefill_workspace_follows_the_two_regimes(L):
-    """Below 16384 tokens the one-call path runs each stage over all heads, so
-    its workspace is the probe workspace of the whole problem; from 16384 on
-    it pipelines over KV-head groups and needs one group's workspace."""
+def test_prefill_workspace_is_the_probe_workspace(L):
+    """The one-call path runs the three stages over the whole layer, so its
+    workspace is the whole problem's probe workspace."""
     t = eb.Tiling(128, 64)
-    short = eb.Dims(2, 32, 8, 8192, 128)
-    assert L.ei_prefill_workspace_bytes(short, t) == L.ei_probe_workspace_bytes(short, t)
-    for n in (16384, 32768, 131072):
-        long_ = eb.Dims(2, 32, 8, n, 128)
-        one = eb.Dims(1, 4, 1, n, 128)
-        assert L.ei_prefill_workspace_bytes(long_, t) == L.ei_probe_workspace_bytes(one, t)
-    # a one-group workspace is too small for a short problem: rejected, nothing launched
-    d = eb.Dims(1, 8, 2, 8192, 128)
-    p = eb.budget_params()
-    km = L.ei_kmax(t, p)
-    ws_one = L.ei_probe_workspace_bytes(eb.Dims(1, 4, 1, 8192, 128), t)
-    assert ws_one < L.ei_prefill_workspace_bytes(d, t)
-    outs = (FAKE,) * 7
-    assert L.ei_entropy_guided_prefill(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, FAKE,
-                                       ws_one, FAKE, FAKE2, FAKE3) == -4
+    for n in (1024, 8192, 16384, 131072):
+        d = eb.Dims(2, 32, 8, n, 128)
+        assert L.ei_prefill_workspace_bytes(d, t) == L.ei_probe_workspace_bytes(d, t) > 0
 
 
 def test_bench_refuses_several_gpus():
@@ -233,14 +214,13 @@ def test_misaligned_pointers_are_refused(L):
     ws = L.ei_prefill_workspace_bytes(d, t)
     call = L.ei_entropy_guided_prefill
     outs = [FAKE] * 7
-    assert call(FAKE, FAKE, _off(FAKE, 2), d, t, 1.0, p, 0, km, 0.088, *outs, FAKE, ws, FAKE,
-                FAKE2, FAKE3) == -3
+    assert call(FAKE, FAKE, _off(FAKE, 2), d, t, 1.0, p, 0, km, 0.088, *outs, FAKE, ws,
+                None) == -3
     bad = list(outs)
     bad[4] = _off(FAKE, 2)   # block_idx
-    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *bad, FAKE, ws, FAKE, FAKE2,
-                FAKE3) == -3
-    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, _off(FAKE, 8), ws, FAKE,
-                FAKE2, FAKE3) == -3
+    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *bad, FAKE, ws, None) == -3
+    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, _off(FAKE, 8), ws,
+                None) == -3
 
 
 def test_sizes_whose_grids_overflow_are_refused(L):
@@ -320,7 +300,7 @@ def test_attention_refuses_non_positive_or_non_finite_scales(L, scale):
     p = eb.budget_params()
     ws = L.ei_prefill_workspace_bytes(d, t)
     assert L.ei_entropy_guided_prefill(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, L.ei_kmax(t, p), scale,
-                                       *(FAKE,) * 7, FAKE, ws, FAKE, FAKE2, FAKE3) == -2
+                                       *(FAKE,) * 7, FAKE, ws, None) == -2
 
 
 @pytest.mark.parametrize("ps", (float("inf"), float("-inf"), float("nan")))
@@ -331,36 +311,26 @@ def test_probe_refuses_non_finite_probe_scale(L, ps):
     p = eb.budget_params()
     ws = L.ei_prefill_workspace_bytes(d, t)
     assert L.ei_entropy_guided_prefill(FAKE, FAKE, FAKE, d, t, ps, p, 0, L.ei_kmax(t, p), 0.088,
-                                       *(FAKE,) * 7, FAKE, ws, FAKE, FAKE2, FAKE3) == -2
-
-
-def test_pipelined_prefill_needs_an_event(L):
-    """From 16384 tokens on the one-call path orders its two streams with the
-    caller's event: a NULL event is EI_ERR_NULL before any launch."""
-    t, p = eb.Tiling(128, 64), eb.budget_params()
-    d = eb.Dims(1, 4, 1, 16384, 128)
-    ws = L.ei_prefill_workspace_bytes(d, t)
-    assert L.ei_entropy_guided_prefill(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, L.ei_kmax(t, p), 0.088,
-                                       *(FAKE,) * 7, FAKE, ws, FAKE, FAKE2, None) == -1
+                                       *(FAKE,) * 7, FAKE, ws, None) == -2
 
 
 def test_noalloc_prefill_refusals(L):
     """ei_entropy_guided_prefill_noalloc validates like the workspace entry
     point and refuses, before touching a device, a problem whose probe
-    workspace exceeds its static scratch array (32 MiB)."""
+    workspace exceeds its static scratch array (128 MiB)."""
     t, p = eb.Tiling(128, 64), eb.budget_params()
     km = L.ei_kmax(t, p)
     call = L.ei_entropy_guided_prefill_noalloc
     outs = (FAKE,) * 7
-    big = eb.Dims(1, 64, 1, 131072, 128)   # one KV group of 64 heads at 128k
-    assert L.ei_prefill_workspace_bytes(big, t) > 32 << 20
-    assert call(FAKE, FAKE, FAKE, big, t, 1.0, p, 0, km, 0.088, *outs, FAKE, FAKE2, FAKE3) == -4
-    d = eb.Dims(1, 4, 1, 16384, 128)
-    assert L.ei_prefill_workspace_bytes(d, t) <= 32 << 20
-    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.0, *outs, FAKE, FAKE2, FAKE3) == -2
-    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, FAKE, FAKE2, None) == -1
-    assert call(None, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, FAKE, FAKE2, FAKE3) == -1
+    big = eb.Dims(1, 64, 8, 262144, 128)   # the Llama-3-70B layer at 256k
+    assert L.ei_prefill_workspace_bytes(big, t) > 128 << 20
+    assert call(FAKE, FAKE, FAKE, big, t, 1.0, p, 0, km, 0.088, *outs, None) == -4
+    for fits in (eb.Dims(1, 32, 8, 131072, 128), eb.Dims(1, 64, 8, 131072, 128)):
+        assert L.ei_prefill_workspace_bytes(fits, t) <= 128 << 20   # the 8B and 70B layers
+    d = eb.Dims(1, 32, 8, 131072, 128)
+    assert call(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.0, *outs, None) == -2
+    assert call(None, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088, *outs, None) == -1
     assert call(FAKE, FAKE, FAKE, eb.Dims(1, 4, 1, 1024, 96), t, 1.0, p, 0, km, 0.088, *outs,
-                FAKE, FAKE2, FAKE3) == -3
+                None) == -3
     assert call(None, None, None, eb.Dims(0, 4, 1, 1024, 128), t, 1.0, p, 0, km, 0.088,
-                *(None,) * 7, FAKE, FAKE2, None) == 0
+                *(None,) * 7, None) == 0

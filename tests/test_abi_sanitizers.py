@@ -12,6 +12,7 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 MAIN = os.path.join(ROOT, "tests", "native", "abi_sanitize_main.cpp")
 API = os.path.join(ROOT, "paper_2606_09508_amd", "csrc", "ei_api.hip")
+NOALLOC = os.path.join(ROOT, "paper_2606_09508_amd", "csrc", "ei_noalloc.hip")
 OBJS = [os.path.join(ROOT, "paper_2606_09508_amd", "_build", f"{n}.o")
         for n in ("ei_probe", "ei_select", "ei_attn")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -24,14 +25,16 @@ def test_abi_host_code_is_clean_under_asan_and_ubsan(tmp_path):
     if not all(os.path.exists(o) for o in OBJS):
         pytest.skip("the library's kernel objects are not built")
     common = ["-O1", "-g", "-std=c++17", "-I", os.path.join(ROOT, "include")]
-    api_o, main_o, exe = (str(tmp_path / n) for n in ("api.o", "main.o", "abi_sanitized"))
+    api_o, na_o, main_o, exe = (str(tmp_path / n)
+                                for n in ("api.o", "noalloc.o", "main.o", "abi_sanitized"))
+    host = [HIPCC, "--offload-arch=gfx950", *common, "-fPIC", "-Xclang", "-target-feature",
+            "-Xclang", "-packed-fp32-ops", *SAN, "-Xarch_host", "-fno-sanitize-recover=all"]
     steps = [
-        [HIPCC, "--offload-arch=gfx950", *common, "-fPIC", "-Xclang", "-target-feature",
-         "-Xclang", "-packed-fp32-ops", *SAN, "-Xarch_host", "-fno-sanitize-recover=all",
-         "-c", API, "-o", api_o],
+        [*host, "-c", API, "-o", api_o],
+        [*host, "-c", NOALLOC, "-o", na_o],
         [HIPCC, *common, *SAN, "-Xarch_host", "-fno-sanitize-recover=all", "-x", "c++", "-c",
          MAIN, "-o", main_o],
-        [HIPCC, "--offload-arch=gfx950", *SAN, main_o, api_o, *OBJS, "-o", exe],
+        [HIPCC, "--offload-arch=gfx950", *SAN, main_o, api_o, na_o, *OBJS, "-o", exe],
     ]
     for cmd in steps:
         r = subprocess.run(cmd, capture_output=True, text=True)

@@ -2,8 +2,7 @@
 static scratch array instead of a caller's workspace) against
 ei_entropy_guided_prefill on the same inputs, bitwise, through the C ABI: two
 calls in a row, the second on a smaller problem (so the scratch array holds
-the first call's larger contents when the second runs), and the pipelined
-and the short regimes both covered."""
+the first call's larger contents when the second runs)."""
 import sys
 
 import numpy as np
@@ -45,8 +44,8 @@ def same(w, a, b):
 def test_noalloc_equals_workspace_entry_point_two_calls():
     """Collected last (test_zz_*): it also passes after every other GPU test
     has run in the same process."""
-    cases = [("c2", 1, dict(N=32768)),          # pipelined over KV-head groups
-             ("c1", 3, dict(Hq=8, Hkv=2, N=4096 + 192))]   # smaller, short regime
+    cases = [("c2", 1, dict(N=32768)),                       # the 8B layer at 32k
+             ("c1", 3, dict(Hq=8, Hkv=2, N=4096 + 192))]   # smaller, ragged
     for wl, seed, case in cases:
         w = synth.make(wl, seed, **case)
         print(f"[noalloc] {wl} seed={seed} {case}", file=sys.stderr, flush=True)
