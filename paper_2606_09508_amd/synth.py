@@ -34,7 +34,10 @@ Workloads (shapes of the layers the paper evaluates, Section 5):
   segment's queries also carry.
 * ``c5`` Llama-3-70B layer on one GPU: Hq=64, Hkv=8, N=131072; an eighth of
   the heads sink everywhere, the others drift between types over 8192-token
-  regions as a Markov chain with stay probability 0.75.
+  regions as a Markov chain with stay probability 0.75.  The always-sink heads
+  carry sink amplitudes spread evenly from 8.25 down to 7.25 (in head order),
+  so that their largest segment entropies straddle the three entropy
+  thresholds the workload is swept over (1e-6, 1e-5, 1e-4).
 """
 from __future__ import annotations
 
@@ -83,6 +86,7 @@ class Workload:
     markov_stay: float = 0.0
     key_lognormal: float = 0.0
     n_spans: int = 0
+    sink_amp: tuple | None = None   # (first, last) C_Q of the always-sink heads
     q: np.ndarray | None = field(default=None, repr=False)
     k: np.ndarray | None = field(default=None, repr=False)
     v: np.ndarray | None = field(default=None, repr=False)
@@ -119,7 +123,8 @@ PRESETS = {
     "c4": dict(B=1, Hq=28, Hkv=4, N=65536, D=128, Ls=128, Lb=64, base_budget=2048,
                recipe="regions", region=2048, key_lognormal=0.5, n_spans=10),
     "c5": dict(B=1, Hq=64, Hkv=8, N=131072, D=128, Ls=128, Lb=64, base_budget=2048,
-               recipe="regions", region=8192, always_sink_frac=0.125, markov_stay=0.75),
+               recipe="regions", region=8192, always_sink_frac=0.125, markov_stay=0.75,
+               sink_amp=(8.25, 7.25)),
 }
 
 # type codes used in Workload.plan
@@ -187,6 +192,21 @@ def _span_plan(w: Workload):
     return spans, dirs
 
 
+def sink_amplitudes(w: Workload) -> np.ndarray:
+    """[B, Hq] query sink amplitude of every head (C_Q unless ``sink_amp``
+    spreads the always-sink heads' amplitudes)."""
+    amp = np.full((w.B, w.Hq), C_Q, np.float64)
+    if w.sink_amp is None or w.plan is None:
+        return amp
+    for b in range(w.B):
+        always = [h for h in range(w.Hq) if (w.plan[b, h] == SINK).all()]
+        n = len(always)
+        for i, h in enumerate(always):
+            f = i / (n - 1) if n > 1 else 0.0
+            amp[b, h] = w.sink_amp[0] + (w.sink_amp[1] - w.sink_amp[0]) * f
+    return amp
+
+
 def generate(w: Workload, heads_q=None) -> Workload:
     """Fill w.q, w.k, w.v (uint16 bf16 bits, [B, H, N, D]) in place and return w.
 
@@ -197,6 +217,7 @@ def generate(w: Workload, heads_q=None) -> Workload:
     B, Hq, Hkv, N, D = w.B, w.Hq, w.Hkv, w.N, w.D
     G = Hq // Hkv
     w.plan = _plan(w)
+    amp = sink_amplitudes(w)
     spans, dirs = _span_plan(w)
     w.spans = spans
     rot_c1 = _rot(N, A_LOCAL_C1)
@@ -229,7 +250,7 @@ def generate(w: Workload, heads_q=None) -> Workload:
                 r0, r1 = r * w.region, min(N, (r + 1) * w.region)
                 t = int(w.plan[b, h, r])
                 if t == SINK:
-                    x[r0:r1, D - 1] = C_Q
+                    x[r0:r1, D - 1] = amp[b, h]
                     if w.recipe == "c1":
                         x[r0:r1, D - 3: D - 1] = rot_c1[r0:r1]
                 elif t == LOCAL:

@@ -592,6 +592,12 @@ def test_c5_llama70b_128k_sampled():
     r = run_path(w)
     hrel, lerr = check_probe(w, r, _sample_rows(w, n_seg=24, seed=4))
     check_select(w, r)
+    # the three thresholds of the sweep classify 4, 6 and 7 heads as rigid
+    # (the oracle's own counts, pinned on the CPU)
+    counts = {e_t: int((r["en"].max(axis=2) < np.float32(e_t)).sum()) for e_t in (1e-6, 1e-5, 1e-4)}
+    say(f"  rigid heads at e_t = 1e-6 / 1e-5 / 1e-4: {counts}")
+    assert counts == {1e-6: 4, 1e-5: 6, 1e-4: 7}
+    assert int(r["sel"]["rigid"].sum()) == counts[1e-5]
     for e_t in (1e-6, 1e-4):
         ls = torch.from_numpy(r["ls"]).cuda()
         en = torch.from_numpy(r["en"]).cuda()
