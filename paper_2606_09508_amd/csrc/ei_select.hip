@@ -20,11 +20,14 @@
 //                 16-bit counters) of the bits below the keys' common prefix
 //                 picks T's bucket (a DPP prefix sum over the lanes' 32-bucket
 //                 groups, then one over the chosen group's buckets); the keys
-//                 of that bucket (usually few) are compacted to one per lane
-//                 and T's remaining bits are resolved there with one ballot
-//                 per bit.  Ties at T keep the highest block indices; the
-//                 chosen blocks plus the segment's own blocks are written
-//                 ascending.
+//                 of that bucket (usually few, at most 128 here) are
+//                 compacted to two per lane and T's remaining bits are
+//                 resolved there with two ballots per bit.  Ties at T keep
+//                 the highest block indices; the chosen blocks plus the
+//                 segment's own blocks are written ascending.  The kernel is
+//                 bound by instruction issue: the row's index is wave-uniform
+//                 and every slot loop tests its slot against the row's length
+//                 as a scalar branch, so no per-slot lane masks are formed.
 #include "../../include/entropyinfer.h"
 #include "ei_internal.h"
 
@@ -125,12 +128,21 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(
 
 // Order-preserving key of a binary32 score, shifted by one so that 0 marks
 // an empty slot: NaN -> 1 (below -inf), -0 == +0, larger float -> larger key.
+// Selects only (no branches).
 __device__ __forceinline__ uint32_t score_key(float v) {
-  if (v != v) return 1u;
-  if (v == 0.0f) v = 0.0f;
-  const uint32_t u = __float_as_uint(v);
+  const uint32_t u = v == 0.0f ? 0u : __float_as_uint(v);
   const uint32_t k = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-  return k + 1u;   // finite/inf keys are <= 0xff800000, so no wrap
+  return (v != v ? 0u : k) + 1u;   // finite/inf keys are <= 0xff800000, so no wrap
+}
+
+__device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
+
+// A copy of a wave-uniform value that the optimizer cannot see through: the
+// slot tests of each loop against it stay scalar branches, instead of lane
+// masks computed once and kept live (in SGPRs, spilled) across the loops.
+__device__ __forceinline__ int fresh_uniform(int x) {
+  asm volatile("" : "+s"(x));
+  return x;
 }
 
 constexpr int kWavesPerGroup = kThreads / kWave;
@@ -145,14 +157,14 @@ __device__ __forceinline__ void wave_lds_fence() {
 }
 
 template <int SLOTS>
-__global__ __launch_bounds__(kThreads) void topk_kernel(
+__global__ __launch_bounds__(kThreads, SLOTS <= 32 ? 6 : 1) void topk_kernel(
     const float* __restrict__ log_scores, const int32_t* __restrict__ kblocks, int64_t rows,
     int CS, int CB, int r, int kmax, int32_t* __restrict__ idx, int32_t* __restrict__ cnt) {
   // per-wave scratch: bucket counts (16-bit halves of 32-bit words: a row has
   // at most 8192 keys) and the compacted keys of T's bucket
   __shared__ __attribute__((aligned(16))) uint32_t hist_all[kWavesPerGroup][kHistBins / 2];
-  __shared__ uint32_t cand_all[kWavesPerGroup][kWave];
-  const int wv = threadIdx.x >> 6;
+  __shared__ uint32_t cand_all[kWavesPerGroup][2 * kWave];
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   const int64_t row = (int64_t)blockIdx.x * kWavesPerGroup + wv;
   if (row >= rows) return;   // no workgroup barriers below
   uint32_t* hist = hist_all[wv];
@@ -181,11 +193,9 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
 #pragma unroll
     for (int sl = 0; sl < SLOTS; ++sl) {
       const int j = sl * kWave + lane;
-      key[sl] = (sl < nsl && j < npast) ? score_key(raw[sl]) : 0u;
-      if (key[sl]) {
-        kmx = key[sl] > kmx ? key[sl] : kmx;
-        kmn = key[sl] < kmn ? key[sl] : kmn;
-      }
+      key[sl] = j < npast ? score_key(raw[sl]) : 0u;   // j < npast: sl < nsl
+      kmx = key[sl] > kmx ? key[sl] : kmx;
+      kmn = (key[sl] != 0u && key[sl] < kmn) ? key[sl] : kmn;
     }
     kmx = wave_max_u32_f(kmx);
     kmn = wave_min_u32_f(kmn);
@@ -205,9 +215,10 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
       const uint32_t dmask = (2u << (top - shift)) - 1u;
       for (int i = lane; i < kHistBins / 8; i += kWave) ((uint4*)hist)[i] = make_uint4(0, 0, 0, 0);
       wave_lds_fence();
+      const int nsh = fresh_uniform(nsl);
 #pragma unroll
       for (int sl = 0; sl < SLOTS; ++sl)
-        if (sl < nsl && key[sl]) {
+        if (sl < nsh && key[sl]) {
           const uint32_t bin = (key[sl] >> shift) & dmask;
           atomicAdd(&hist[bin >> 1], 1u << (16 * (bin & 1)));
         }
@@ -224,7 +235,7 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
       const uint32_t pre = wave_incl_scan_u32(S);   // inclusive prefix over lanes
       const uint32_t total = rl_u32(pre, kWave - 1);
       const uint32_t suf = total - pre + S;   // keys in buckets of lanes >= lane
-      const uint64_t okm = __ballot(suf >= (uint32_t)kk);
+      const uint64_t okm = ballot(suf >= (uint32_t)kk);
       const int ls = 63 - __clzll(okm);     // okm != 0: total = npast > kk
       // lane ls's 32 buckets, highest first, one per lane t < 32: T's bucket
       // is the first at which the keys above ls's buckets plus the running
@@ -236,7 +247,7 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
         bt = (hist[bin >> 1] >> (16 * (bin & 1))) & 0xffffu;
       }
       const uint32_t run = wave_incl_scan_u32(bt);
-      const uint64_t hit = __ballot(lane < 32 && acc0 + run >= (uint32_t)kk);
+      const uint64_t hit = ballot(lane < 32 && acc0 + run >= (uint32_t)kk);
       const int tb = (int)__builtin_ctzll(hit);
       const int dstar = 32 * ls + 31 - tb;
       const uint32_t above = acc0 + rl_u32(run - bt, tb);
@@ -245,33 +256,37 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
       if (shift == 0) {
         gt = (int)above;
         eq = (int)nb;
-      } else if (nb <= (uint32_t)kWave) {
-        // compact the bucket's keys, one per lane, and resolve the low bits
+      } else if (nb <= (uint32_t)(2 * kWave)) {
+        // compact the bucket's keys, two per lane, and resolve the low bits
         int cp = 0;
+        const int nsc = fresh_uniform(nsl);
 #pragma unroll
         for (int sl = 0; sl < SLOTS; ++sl) {
-          if (sl >= nsl) break;
-          const bool in = key[sl] != 0u && ((key[sl] >> shift) & dmask) == (uint32_t)dstar;
-          const uint64_t m = __ballot(in);
-          if (in) cand[cp + popc64(m & lt_mask)] = key[sl];
-          cp += popc64(m);
+          if (sl < nsc) {
+            const bool in = key[sl] != 0u && ((key[sl] >> shift) & dmask) == (uint32_t)dstar;
+            const uint64_t m = ballot(in);
+            if (in) cand[cp + popc64(m & lt_mask)] = key[sl];
+            cp += popc64(m);
+          }
         }
         wave_lds_fence();
-        const uint32_t ck = lane < (int)nb ? cand[lane] : 0u;
+        const uint32_t c0 = lane < (int)nb ? cand[lane] : 0u;
+        const uint32_t c1 = lane + kWave < (int)nb ? cand[lane + kWave] : 0u;
         for (int bit = shift - 1; bit >= 0; --bit) {
           const uint32_t c = T | (1u << bit);
-          if ((int)above + popc64(__ballot(ck >= c)) >= kk) T = c;
+          if ((int)above + popc64(ballot(c0 >= c)) + popc64(ballot(c1 >= c)) >= kk) T = c;
         }
-        gt = (int)above + popc64(__ballot(ck > T));
-        eq = popc64(__ballot(ck == T));
+        gt = (int)above + popc64(ballot(c0 > T)) + popc64(ballot(c1 > T));
+        eq = popc64(ballot(c0 == T)) + popc64(ballot(c1 == T));
       } else {
         // large bucket (many equal high bits): resolve over all slots
         for (int bit = shift - 1; bit >= 0; --bit) {
           const uint32_t c = T | (1u << bit);
           int n = 0;
+          const int nsb = fresh_uniform(nsl);
 #pragma unroll
           for (int sl = 0; sl < SLOTS; ++sl)
-            if (sl < nsl) n += popc64(__ballot(key[sl] >= c));
+            if (sl < nsb) n += popc64(ballot(key[sl] >= c));
           if (n >= kk) T = c;
         }
       }
@@ -279,34 +294,67 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(
     if (gt < 0) {
       gt = 0;
       eq = 0;
+      const int nse = fresh_uniform(nsl);
 #pragma unroll
       for (int sl = 0; sl < SLOTS; ++sl)
-        if (sl < nsl) {
-          gt += popc64(__ballot(key[sl] > T));
-          eq += popc64(__ballot(key[sl] == T));
+        if (sl < nse) {
+          gt += popc64(ballot(key[sl] > T));
+          eq += popc64(ballot(key[sl] == T));
         }
     }
     const int need = kk - gt;   // 1 .. eq keys equal to T, highest indices first
     int J = 0;
     if (need < eq) {
+      // J = the largest index with at least `need` keys equal to T at or
+      // above it.  The lane's slots holding T as a bit mask, so that the
+      // search keeps no per-slot wave masks live.
+      constexpr int kWords = (SLOTS + 31) / 32;
+      uint32_t tm[kWords];
+#pragma unroll
+      for (int w = 0; w < kWords; ++w) tm[w] = 0u;
+      const int nst = fresh_uniform(nsl);
+#pragma unroll
+      for (int sl = 0; sl < SLOTS; ++sl)
+        if (sl < nst && key[sl] == T) tm[sl / 32] |= 1u << (sl % 32);
       const int top = 31 - __clz(max(npast - 1, 1));
       for (int bit = top; bit >= 0; --bit) {
         const int c = J | (1 << bit);
-        int n = 0;
+        const int cs = c / kWave, cl = c % kWave;   // index c = slot cs, lane cl
+        uint32_t nl = 0;
 #pragma unroll
-        for (int sl = 0; sl < SLOTS; ++sl)
-          if (sl < nsl) n += popc64(__ballot(key[sl] == T && sl * kWave + lane >= c));
-        if (n >= need) J = c;
+        for (int w = 0; w < kWords; ++w) {
+          const int lo = cs - 32 * w;   // slots of word w above cs: bits > lo
+          const uint32_t above =
+              lo < 0 ? 0xffffffffu : (lo >= 31 ? 0u : ~((2u << lo) - 1u));
+          nl += __popc(tm[w] & above);
+          if (lo >= 0 && lo < 32 && lane >= cl) nl += (tm[w] >> lo) & 1u;
+        }
+        if ((int)rl_u32(wave_incl_scan_u32(nl), kWave - 1) >= need) J = c;
       }
     }
+    // the picks, ascending; J = 0 (the common case) takes every key >= T
+    const int nsp = fresh_uniform(nsl);
+    if (J == 0) {
 #pragma unroll
-    for (int sl = 0; sl < SLOTS; ++sl) {
-      if (sl >= nsl) break;
-      const int j = sl * kWave + lane;
-      const bool pick = key[sl] > T || (key[sl] == T && j >= J);
-      const uint64_t m = __ballot(pick);
-      if (pick) out[pos + popc64(m & lt_mask)] = j;
-      pos += popc64(m);
+      for (int sl = 0; sl < SLOTS; ++sl) {
+        if (sl < nsp) {
+          const bool pick = key[sl] >= T;
+          const uint64_t m = ballot(pick);
+          if (pick) out[pos + popc64(m & lt_mask)] = sl * kWave + lane;
+          pos += popc64(m);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int sl = 0; sl < SLOTS; ++sl) {
+        if (sl < nsp) {
+          const int j = sl * kWave + lane;
+          const bool pick = key[sl] > T || (key[sl] == T && j >= J);
+          const uint64_t m = ballot(pick);
+          if (pick) out[pos + popc64(m & lt_mask)] = j;
+          pos += popc64(m);
+        }
+      }
     }
   }
   const int dend = min((s + 1) * r, CB);
