@@ -334,3 +334,19 @@ def test_noalloc_prefill_refusals(L):
                 None) == -3
     assert call(None, None, None, eb.Dims(0, 4, 1, 1024, 128), t, 1.0, p, 0, km, 0.088,
                 *(None,) * 7, None) == 0
+
+@pytest.mark.parametrize("n,tiling", [(1000, (128, 64)), (1, (128, 64)), (130, (256, 128)),
+                                      (131071, (128, 64))])
+def test_ragged_sequence_lengths_are_accepted(L, n, tiling):
+    """N need not be a multiple of L_S or L_B (a deliberate superset of the
+    boundary's shape rule): the shape checks pass and the call stops at the
+    next check, the missing workspace, before anything is launched."""
+    d, t = eb.Dims(1, 4, 1, n, 128), eb.Tiling(*tiling)
+    assert L.ei_num_segments(d, t) == -(-n // t.seg_len)
+    assert L.ei_num_blocks(d, t) == -(-n // t.block_len)
+    assert L.ei_probe_workspace_bytes(d, t) > 0
+    assert L.ei_entropy_probe(FAKE, FAKE, d, t, 1.0, FAKE, FAKE, FAKE, 0, None) == -4
+    p = eb.budget_params()
+    km = L.ei_kmax(t, p)
+    assert L.ei_entropy_guided_prefill(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088,
+                                       *((FAKE,) * 7), FAKE, 0, None) == -4

@@ -675,3 +675,40 @@ def test_one_call_prefill_c2_repeated():
         torch.cuda.synchronize()
         assert torch.equal(o, o2) and torch.equal(en, en2)
         assert torch.equal(sel["idx"], sel2["idx"])
+
+
+def _end_to_end_agreement(w, r):
+    """Informational (not a parity bar): the oracle's own probe (binary64,
+    rounded to binary32 as the GPU stores it) fed to the oracle's selection,
+    against the GPU's selection.  Returns (fraction of (b, h, s) rows whose
+    block list differs, fraction of heads whose rigid flag differs, fraction
+    of rows whose budget differs)."""
+    Lr, Hr = oracle.probe(w.q, w.k, w.Ls, w.Lb, w.probe_scale)
+    ls = np.nan_to_num(Lr, nan=-np.inf).astype(np.float32)
+    en = Hr.astype(np.float32)
+    del Lr
+    ref = oracle.select(ls, en, w.N, w.Ls, w.Lb, w.e_t, w.alpha, w.delta_t, w.base_budget,
+                        w.mult)
+    g = r["sel"]
+    rows_diff = float(np.any(g["idx"] != ref["idx"], axis=-1).mean())
+    rigid_diff = float((g["rigid"] != ref["rigid"]).mean())
+    budget_diff = float((g["budget"] != ref["budget"]).mean())
+    return rows_diff, rigid_diff, budget_diff
+
+
+@pytest.mark.parametrize("wl", ["c2", "c3"])
+def test_end_to_end_selection_agreement(wl, c3):
+    """The selection the whole oracle path (probe -> select) makes against
+    the GPU's, reported: rows whose block list differs, rigid flags and
+    budgets.  Near-ties of fp32 scores can order differently after the
+    probe's rounding, so this is not bit-exact by construction; the
+    bit-exact bar is the selection on the GPU's own scores."""
+    if wl == "c3":
+        w, r = c3
+    else:
+        w = synth.make("c2", 0)
+        r = run_path(w)
+    rows_diff, rigid_diff, budget_diff = _end_to_end_agreement(w, r)
+    say(f"  [{wl}] end-to-end: block lists differ on {rows_diff:.4%} of rows, rigid flags on "
+        f"{rigid_diff:.4%} of heads, budgets on {budget_diff:.4%} of rows")
+    assert rows_diff < 0.05 and rigid_diff == 0.0
