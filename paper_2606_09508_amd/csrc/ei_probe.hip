@@ -412,7 +412,10 @@ __global__ __launch_bounds__(kThreads, 4) void scores_kernel(
   // The residual part of the 16 logits per row of tile kt and key tile t, if
   // its bound can reach tau: bf16 MFMA with rows (unit, vector, 0 / pad) and
   // the operand [q_r | q_g] . [k | k_r].  corr[bk][2 a] is the lane's value.
-  auto residual = [&](int kt, int t, f32x4 (&corr)[2]) {
+  // A half whose bound is zero (no residual bits in the row tile's query
+  // vectors, or in the tile's key vectors) only adds exact zeros and is
+  // skipped; do_q / do_k are wave-uniform.
+  auto residual = [&](int kt, int t, f32x4 (&corr)[2], bool do_q, bool do_k) {
     corr[0] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
     corr[1] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
     const int ui = u0 + 4 * KT * wave + 4 * kt + (col >> 2);
@@ -424,6 +427,7 @@ __global__ __launch_bounds__(kThreads, 4) void scores_kernel(
         kcorr + (size_t)__builtin_amdgcn_readfirstlane(t) * kKCorrTile;
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) {
+      if (kk < 4 ? !do_q : !do_k) continue;   // kk 0-3: <q_r, k>; 4-7: <q_g, k_r>
       const uint4 qa = has ? *(const uint4*)(qc + 32 * kk + 8 * gq) : make_uint4(0, 0, 0, 0);
 #pragma unroll
       for (int bk = 0; bk < 2; ++bk) {
@@ -463,7 +467,8 @@ __global__ __launch_bounds__(kThreads, 4) void scores_kernel(
     }
     if (__builtin_amdgcn_ballot_w64(need) != 0) {
       f32x4 corr[2];
-      residual(kt, t, corr);
+      residual(kt, t, corr, __builtin_amdgcn_ballot_w64(Rqm[kt] > 0.0f) != 0,
+               __builtin_amdgcn_ballot_w64(k0.R > 0.0f || k1.R > 0.0f) != 0);
 #pragma unroll
       for (int a = 0; a < 2; ++a)
 #pragma unroll
