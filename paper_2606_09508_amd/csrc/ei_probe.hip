@@ -310,6 +310,7 @@ constexpr int kThreads = 256;                       // 4 waves
 constexpr int KT = 1;
 constexpr int kUnits = kThreads / kWave * 4 * KT;
 constexpr int kStageBytes = kKLimbTile + kKMetaTile;
+constexpr int kTilesPerStep = 2;    // key tiles staged per barrier
 
 __device__ __forceinline__ float hw_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float hw_log2(float x) { return __builtin_amdgcn_logf(x); }
@@ -340,7 +341,7 @@ __global__ __launch_bounds__(kThreads, 4) void scores_kernel(
     const unsigned char* __restrict__ ws, Layout lay, float* __restrict__ log_scores,
     float* __restrict__ entropy, int Hq, int Hkv, int CS, int CB, int CBt, int r, int n_groups,
     int n_chunks, double ps_abs, double sgn, float tau) {
-  __shared__ __attribute__((aligned(16))) unsigned char stage[2][kStageBytes];
+  __shared__ __attribute__((aligned(16))) unsigned char stage[2][kTilesPerStep * kStageBytes];
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
   const int gq = lane >> 4, col = lane & 15;
@@ -476,19 +477,29 @@ __global__ __launch_bounds__(kThreads, 4) void scores_kernel(
     }
   };
 
-  // key tile staging: two LDS buffers, the next tile held in registers
-  uint4 p0, p1, pm;
-  auto load_tile = [&](int t) {
-    const uint4* src = (const uint4*)(klimb + (size_t)t * kKLimbTile);
-    p0 = src[tid];
-    p1 = src[kThreads + tid];
-    if (tid < kKMetaTile / 16) pm = ((const uint4*)(kmeta + (size_t)t * kKMetaTile))[tid];
+  // Key tile staging: two LDS buffers of kTilesPerStep tiles each, the next
+  // step's tiles held in registers (a slot past the last tile repeats the
+  // last tile, unread).
+  i32x4 p0[kTilesPerStep], p1[kTilesPerStep], pm[kTilesPerStep];
+  const int n_steps = (nt + kTilesPerStep - 1) / kTilesPerStep;
+  auto load_step = [&](int i) {
+#pragma unroll
+    for (int k = 0; k < kTilesPerStep; ++k) {
+      const int t = min(kTilesPerStep * i + k, nt - 1);
+      const i32x4* src = (const i32x4*)(klimb + (size_t)t * kKLimbTile);
+      p0[k] = src[tid];
+      p1[k] = src[kThreads + tid];
+      if (tid < kKMetaTile / 16) pm[k] = ((const i32x4*)(kmeta + (size_t)t * kKMetaTile))[tid];
+    }
   };
-  auto store_tile = [&](int buf) {
-    uint4* dst = (uint4*)stage[buf];
-    dst[tid] = p0;
-    dst[kThreads + tid] = p1;
-    if (tid < kKMetaTile / 16) dst[kKLimbTile / 16 + tid] = pm;
+  auto store_step = [&](int buf) {
+#pragma unroll
+    for (int k = 0; k < kTilesPerStep; ++k) {
+      i32x4* dst = (i32x4*)(stage[buf] + k * kStageBytes);
+      dst[tid] = p0[k];
+      dst[kThreads + tid] = p1[k];
+      if (tid < kKMetaTile / 16) dst[kKLimbTile / 16 + tid] = pm[k];
+    }
   };
 
   // pass 1 state per row tile, query vector a and key vector bk
@@ -509,12 +520,16 @@ __global__ __launch_bounds__(kThreads, 4) void scores_kernel(
   // tiles below nv_min are visible to every unit of the workgroup (when all
   // its units exist: a unit past the group's last has no row at all)
   const int nv_min = u0 + kUnits <= U ? min((u0 / G + 1) * r, CB) : 0;
-  load_tile(0);
-  store_tile(0);
-  if (nt > 1) load_tile(1);
+  load_step(0);
+  store_step(0);
+  if (n_steps > 1) load_step(1);
   __syncthreads();
-  for (int t = 0; t < nt; ++t) {
-    const unsigned char* st = stage[t & 1];
+  for (int i = 0; i < n_steps; ++i) {
+#pragma unroll
+  for (int k = 0; k < kTilesPerStep; ++k) {
+    const int t = kTilesPerStep * i + k;
+    if (t >= nt) continue;
+    const unsigned char* st = stage[i & 1] + k * kStageBytes;
     const int j = kTileBlocks * t + col;
     const bool whole = kTileBlocks * (t + 1) <= nv_min;   // workgroup-uniform
 #pragma unroll
@@ -542,9 +557,10 @@ __global__ __launch_bounds__(kThreads, 4) void scores_kernel(
           bj_[kt][a][bk] = gt ? j : bj_[kt][a][bk];
         }
     }
-    if (t + 1 < nt) {
-      store_tile((t + 1) & 1);
-      if (t + 2 < nt) load_tile(t + 2);
+  }
+    if (i + 1 < n_steps) {
+      store_step((i + 1) & 1);
+      if (i + 2 < n_steps) load_step(i + 2);
     }
     __syncthreads();
   }
@@ -591,12 +607,16 @@ __global__ __launch_bounds__(kThreads, 4) void scores_kernel(
   float H2[KT];
 #pragma unroll
   for (int kt = 0; kt < KT; ++kt) H2[kt] = 0.0f;
-  load_tile(0);
-  store_tile(0);
-  if (nt > 1) load_tile(1);
+  load_step(0);
+  store_step(0);
+  if (n_steps > 1) load_step(1);
   __syncthreads();
-  for (int t = 0; t < nt; ++t) {
-    const unsigned char* st = stage[t & 1];
+  for (int i = 0; i < n_steps; ++i) {
+#pragma unroll
+  for (int k = 0; k < kTilesPerStep; ++k) {
+    const int t = kTilesPerStep * i + k;
+    if (t >= nt) continue;
+    const unsigned char* st = stage[i & 1] + k * kStageBytes;
     const int j = kTileBlocks * t + col;
     const bool whole = kTileBlocks * (t + 1) <= nv_min;   // workgroup-uniform
 #pragma unroll
@@ -625,9 +645,10 @@ __global__ __launch_bounds__(kThreads, 4) void scores_kernel(
         H2[kt] += h;
       }
     }
-    if (t + 1 < nt) {
-      store_tile((t + 1) & 1);
-      if (t + 2 < nt) load_tile(t + 2);
+  }
+    if (i + 1 < n_steps) {
+      store_step((i + 1) & 1);
+      if (i + 2 < n_steps) load_step(i + 2);
     }
     __syncthreads();
   }
