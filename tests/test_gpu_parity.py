@@ -411,6 +411,58 @@ def test_select_crafted_scores():
             np.testing.assert_array_equal(g[name], ref[name], err_msg=f"{name} B_h={bh}")
 
 
+def _crafted_large_scores(CS, CB, seed=7):
+    """Rows for the wide selector instances (32 to 128 slots per lane): a
+    cluster of 100 keys that share every bit above their low 12 (T's bucket
+    then holds 65..128 keys: the two-per-lane compaction), a cluster of 300
+    (more than 128: the resolution over all slots), 200 keys exactly equal
+    to the row's maximum (ties at T: the index search), over a low random
+    background; and a row type with NaN / +-inf / +-0."""
+    rng = np.random.default_rng(seed)
+    shape = (CS, CB)
+    ls = np.empty((1, 4, CS, CB), np.float32)
+    for h, n in ((0, 100), (1, 300)):
+        x = (rng.standard_normal(shape) - 10.0).astype(np.float32)
+        for s in range(CS):
+            pos = rng.choice(CB, size=min(n, CB), replace=False)
+            x[s, pos] = (0x3F800000 + rng.integers(0, 1 << 12, pos.size)).astype(
+                np.uint32).view(np.float32)
+        ls[0, h] = x
+    x = (rng.standard_normal(shape) - 10.0).astype(np.float32)
+    for s in range(CS):
+        x[s, rng.choice(CB, size=min(200, CB), replace=False)] = 1.0
+    ls[0, 2] = x
+    x = rng.standard_normal(shape).astype(np.float32)
+    u = rng.random(shape)
+    x[u < 0.05] = np.nan
+    x[(u >= 0.05) & (u < 0.1)] = -np.inf
+    x[(u >= 0.1) & (u < 0.12)] = np.inf
+    x[(u >= 0.12) & (u < 0.14)] = -0.0
+    x[(u >= 0.14) & (u < 0.16)] = 0.0
+    ls[0, 3] = x
+    en = rng.uniform(0.5, 1.5, (1, 4, CS)).astype(np.float32)
+    return ls, en
+
+
+@pytest.mark.parametrize("N", [131072, 524288])
+def test_select_crafted_large_rows(N):
+    """The 32- and 128-slot selector instances, bit-exact against the oracle
+    on crafted rows (large threshold buckets, ties at T, NaN / inf / +-0),
+    with budgets that keep 32..96 and up to 384 past blocks."""
+    Ls, Lb = 128, 64
+    CS, CB = N // Ls, N // Lb
+    ls, en = _crafted_large_scores(CS, CB)
+    for bh, mult in ((2048, 3), (8192, 3)):
+        sel = eb.select_blocks(torch.from_numpy(ls).cuda(), torch.from_numpy(en).cuda(), N, Ls,
+                               Lb, 1e-5, 0.5, 0.4, bh, mult, n_kv_heads=4)
+        torch.cuda.synchronize()
+        g = {kk: t.cpu().numpy() for kk, t in sel.items()}
+        ref = oracle.select(ls, en, N, Ls, Lb, 1e-5, 0.5, 0.4, bh, mult)
+        for name in ("rigid", "budget", "cnt", "idx"):
+            np.testing.assert_array_equal(g[name], ref[name], err_msg=f"{name} N={N} B_h={bh}")
+        del sel, g, ref
+
+
 def test_budget_recurrence_across_chunks():
     """Alg. 3's recurrence over more segments than one pass of the budget
     kernel holds (1024): 2085 segments, so B is carried across two chunk
