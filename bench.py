@@ -292,6 +292,35 @@ def main():
                  "bitwise_equal_to_per_head": bool(torch.equal(ou, bufs["out"]))}
         del ou
 
+    # fused probe -> select (ln A never in memory) on the same inputs: time
+    # against the separate probe + select stages, and bitwise agreement
+    fused = None
+    fbufs = {}
+
+    def fstep():
+        eb.probe_select_fused(q, k, w.Ls, w.Lb, w.e_t, w.alpha, w.delta_t, w.base_budget,
+                              w.mult, w.probe_scale, bufs=fbufs)
+
+    try:
+        fstep()
+    except eb.EIError as e:
+        if e.status != -3:   # EI_ERR_UNSUPPORTED: rows longer than its LDS rows
+            raise
+    else:
+        torch.cuda.synchronize()
+        fe = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(10)]
+        for e in fe:
+            e[0].record()
+            fstep()
+            e[1].record()
+        torch.cuda.synchronize()
+        same = torch.equal(fbufs["entropy"], bufs["entropy"]) and all(
+            torch.equal(fbufs[n], bufs["sel"][n]) for n in ("rigid", "budget", "idx", "cnt"))
+        fused = {"ms": round(float(np.median([e[0].elapsed_time(e[1]) for e in fe])), 4),
+                 "separate_probe_plus_select_ms": round(probe_ms + select_ms, 4),
+                 "bitwise_equal_to_separate": bool(same)}
+        del fbufs
+
     cnt = bufs["sel"]["cnt"].cpu().numpy()
     idx = bufs["sel"]["idx"].cpu().numpy()
     rigid = bufs["sel"]["rigid"].cpu().numpy()
@@ -358,6 +387,7 @@ def main():
         "mfma_busy_counter": read_counter_file(SQ_FILE, "mfma_busy_fraction",
                                                 (args.workload, args.seed)),
         "sparse_attn_gqa_union": union,
+        "probe_select_fused": fused,
         "dense_ms": round(dense_ms, 3),
         "dense_tflops": round(dense_tflops, 2),
         "speedup_vs_dense": round(dense_ms / pipe_ms, 3),

@@ -7,6 +7,7 @@
  *   ei_select_blocks        Algorithm 3 (rigid / dynamic heads, budgets) and
  *                           per-segment top-k key-block selection (Section 4.2,
  *                           Appendix A Eq. t_topk)
+ *   ei_probe_select_fused   the two above without ln A in memory
  *   ei_sparse_prefill_attn  causal GQA attention over the selected blocks
  *                           (Appendix A Eq. t_spa); _gqa_union: the same with
  *                           two query heads of a KV group per tile
@@ -198,6 +199,38 @@ ei_status ei_select_blocks_mode(const float* log_scores, const float* entropy, e
                                 ei_tiling tiling, ei_budget_params params, int32_t mode,
                                 int32_t kmax, uint8_t* head_is_rigid, int32_t* budget_blocks,
                                 int32_t* block_idx, int32_t* block_cnt, void* stream);
+
+/* Workspace bytes ei_probe_select_fused needs: ei_probe_workspace_bytes plus
+ * 64 bytes per (b, h, s) of softmax statistics; 0 on invalid sizes. */
+size_t ei_probe_select_workspace_bytes(ei_dims dims, ei_tiling tiling);
+
+/*
+ * ei_probe_select_fused -- ei_entropy_probe followed by ei_select_blocks_mode
+ * without the observation matrix ln A in memory (Appendix A: the top-k of
+ * Eq. t_topk consumes the C_S x C_B matrix of Eq. t_obs; Section 5's latency
+ * study puts the method's extra cost on its per-head work).  After pooling:
+ * the entropies, with each (b, h, s) row's softmax statistics kept in the
+ * workspace; the classification and budgets of Algorithm 3; then the logits
+ * formed once more, ln A of the past blocks held in LDS and the top-k taken
+ * there.  entropy, head_is_rigid, budget_blocks, block_idx and block_cnt are
+ * bitwise those of the two calls with the same arguments.
+ *
+ *   q, k, probe_scale    as ei_entropy_probe
+ *   params, mode, kmax   as ei_select_blocks_mode
+ *   entropy, head_is_rigid, budget_blocks, block_idx, block_cnt
+ *                        out, as the two calls (ln A is not produced)
+ *   workspace            at least ei_probe_select_workspace_bytes()
+ *
+ * Errors: those of the two calls; EI_ERR_UNSUPPORTED also when a segment has
+ * more than 2048 past blocks ((C_S - 1) L_S / L_B > 2048: the LDS rows of the
+ * selection kernel hold at most that many).
+ */
+ei_status ei_probe_select_fused(const uint16_t* q, const uint16_t* k, ei_dims dims,
+                                ei_tiling tiling, double probe_scale, ei_budget_params params,
+                                int32_t mode, int32_t kmax, float* entropy,
+                                uint8_t* head_is_rigid, int32_t* budget_blocks,
+                                int32_t* block_idx, int32_t* block_cnt, void* workspace,
+                                size_t workspace_bytes, void* stream);
 
 /*
  * ei_sparse_prefill_attn -- block-sparse causal GQA attention (Section 4.2,

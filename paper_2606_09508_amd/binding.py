@@ -76,6 +76,12 @@ def lib() -> ctypes.CDLL:
         L.ei_select_blocks_mode.restype = ctypes.c_int
         L.ei_select_blocks_mode.argtypes = [_VP, _VP, Dims, Tiling, BudgetParams, ctypes.c_int32,
                                             ctypes.c_int32, _VP, _VP, _VP, _VP, _VP]
+        L.ei_probe_select_workspace_bytes.restype = ctypes.c_size_t
+        L.ei_probe_select_workspace_bytes.argtypes = [Dims, Tiling]
+        L.ei_probe_select_fused.restype = ctypes.c_int
+        L.ei_probe_select_fused.argtypes = [_VP, _VP, Dims, Tiling, ctypes.c_double, BudgetParams,
+                                            ctypes.c_int32, ctypes.c_int32, _VP, _VP, _VP, _VP,
+                                            _VP, _VP, ctypes.c_size_t, _VP]
         L.ei_sparse_prefill_attn.restype = ctypes.c_int
         L.ei_sparse_prefill_attn.argtypes = [_VP, _VP, _VP, Dims, Tiling, ctypes.c_float, _VP,
                                              _VP, ctypes.c_int32, _VP, _VP]
@@ -255,6 +261,48 @@ def select_blocks(log_scores, entropy, seq_len: int, seg_len: int, block_len: in
                                          _ptr(out["idx"]), _ptr(out["cnt"]), _stream(log_scores))
     _check("ei_select_blocks_mode", st)
     return out
+
+
+def probe_select_workspace_bytes(dims: Dims, seg_len: int, block_len: int) -> int:
+    return int(lib().ei_probe_select_workspace_bytes(dims, Tiling(seg_len, block_len)))
+
+
+def probe_select_fused(q, k, seg_len: int, block_len: int, e_t: float = 1e-5,
+                       alpha: float = 0.5, delta_t: float = 0.4, base_budget: int = 2048,
+                       mult: int = 3, probe_scale: float = 1.0, mode: int = CLASSIFY_HEAD,
+                       kmax_: int | None = None, bufs: dict | None = None):
+    """ei_probe_select_fused (probe and selection without ln A in memory):
+    returns (entropy fp32 [B,Hq,C_S], dict(rigid, budget, idx, cnt) as
+    select_blocks).  ``bufs`` (optional) caches the outputs and workspace."""
+    _req(q, "q", torch.bfloat16, 4)
+    _req(k, "k", torch.bfloat16, 4)
+    check_qkv_shapes(q.shape, k.shape)
+    _same_device(q, k)
+    d = dims_of(q, k)
+    B, Hq, N, _ = q.shape
+    CS = num_segments(N, seg_len)
+    km = kmax(seg_len, block_len, base_budget, mult) if kmax_ is None else int(kmax_)
+    dev = q.device
+    bufs = {} if bufs is None else bufs
+    shapes = {"entropy": ((B, Hq, CS), torch.float32), "rigid": ((B, Hq), torch.uint8),
+              "budget": ((B, Hq, CS), torch.int32), "idx": ((B, Hq, CS, km), torch.int32),
+              "cnt": ((B, Hq, CS), torch.int32)}
+    for name, (shape, dtype) in shapes.items():
+        t = bufs.get(name)
+        if t is None or tuple(t.shape) != shape or t.dtype != dtype or t.device != dev:
+            bufs[name] = torch.empty(shape, dtype=dtype, device=dev)
+    need = max(probe_select_workspace_bytes(d, seg_len, block_len), 1)
+    ws = bufs.get("workspace")
+    if ws is None or ws.numel() < need or ws.device != dev:
+        bufs["workspace"] = ws = torch.empty((need,), dtype=torch.uint8, device=dev)
+    with torch.cuda.device(dev):
+        st = lib().ei_probe_select_fused(
+            _ptr(q), _ptr(k), d, Tiling(seg_len, block_len), float(probe_scale),
+            budget_params(e_t, alpha, delta_t, base_budget, mult), int(mode), km,
+            _ptr(bufs["entropy"]), _ptr(bufs["rigid"]), _ptr(bufs["budget"]), _ptr(bufs["idx"]),
+            _ptr(bufs["cnt"]), _ptr(ws), ws.numel(), _stream(q))
+    _check("ei_probe_select_fused", st)
+    return bufs["entropy"], {n: bufs[n] for n in ("rigid", "budget", "idx", "cnt")}
 
 
 def sparse_prefill_attn(q, k, v, block_idx, block_cnt, seg_len: int, block_len: int,

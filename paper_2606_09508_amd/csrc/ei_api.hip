@@ -10,7 +10,7 @@
 
 namespace {
 
-constexpr int32_t kAbiVersion = 5;
+constexpr int32_t kAbiVersion = 6;
 
 struct Sizes {
   int64_t B, Hq, Hkv, N, D, CS, CB, r;
@@ -175,6 +175,48 @@ ei_status ei_select_blocks_mode(const float* log_scores, const float* entropy, e
   if (!ei::select_supported(ss)) return EI_ERR_UNSUPPORTED;
   return from_hip(ei::launch_select(log_scores, entropy, ss, head_is_rigid, budget_blocks,
                                     block_idx, block_cnt, (hipStream_t)stream));
+}
+
+size_t ei_probe_select_workspace_bytes(ei_dims dims, ei_tiling tiling) {
+  if (check_dims(dims) != EI_OK || check_tiling(tiling) != EI_OK) return 0;
+  const Sizes z = sizes(dims, &tiling);
+  const ei::ProbeShape ps{(int)z.B, (int)z.Hq, (int)z.Hkv, (int)z.N, tiling.seg_len,
+                          tiling.block_len, (int)z.CS, (int)z.CB, (int)z.r};
+  return ei::probe_select_workspace_bytes(ps);
+}
+
+ei_status ei_probe_select_fused(const uint16_t* q, const uint16_t* k, ei_dims dims,
+                                ei_tiling tiling, double probe_scale, ei_budget_params params,
+                                int32_t mode, int32_t kmax, float* entropy,
+                                uint8_t* head_is_rigid, int32_t* budget_blocks,
+                                int32_t* block_idx, int32_t* block_cnt, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+  ei_status st = check_dims(dims);
+  if (st != EI_OK) return st;
+  if ((st = check_tiling(tiling)) != EI_OK) return st;
+  if ((st = check_params(params)) != EI_OK) return st;
+  if (mode < EI_CLASSIFY_HEAD || mode > EI_CLASSIFY_SEGMENT) return EI_ERR_SHAPE;
+  if (!probe_scale_ok(probe_scale)) return EI_ERR_SHAPE;
+  if (kmax < kmax_of(tiling, params)) return EI_ERR_SHAPE;
+  const Sizes z = sizes(dims, &tiling);
+  if (z.B == 0 || z.N == 0) return EI_OK;
+  if (!q || !k || !entropy || !head_is_rigid || !budget_blocks || !block_idx || !block_cnt)
+    return EI_ERR_NULL;
+  if (!aligned16({q, k}) || !aligned4({entropy, budget_blocks, block_idx, block_cnt}))
+    return EI_ERR_UNSUPPORTED;
+  const ei::ProbeShape ps{(int)z.B, (int)z.Hq, (int)z.Hkv, (int)z.N, tiling.seg_len,
+                          tiling.block_len, (int)z.CS, (int)z.CB, (int)z.r};
+  const ei::SelectShape ss{(int)z.B, (int)z.Hq, (int)z.N, tiling.seg_len, tiling.block_len,
+                           (int)z.CS, (int)z.CB, (int)z.r, kmax, params.entropy_threshold,
+                           params.alpha, params.delta_t, params.base_budget_tokens,
+                           params.max_budget_mult, (int)mode, (int)(z.Hq / z.Hkv)};
+  if (!ei::probe_supported(ps) || !ei::probe_select_supported(ps)) return EI_ERR_UNSUPPORTED;
+  if (!workspace || workspace_bytes < ei::probe_select_workspace_bytes(ps))
+    return EI_ERR_WORKSPACE;
+  if (!aligned16({workspace})) return EI_ERR_UNSUPPORTED;
+  return from_hip(ei::launch_probe_select(q, k, ps, probe_scale, ss, entropy, head_is_rigid,
+                                          budget_blocks, block_idx, block_cnt, workspace,
+                                          (hipStream_t)stream));
 }
 
 ei_status ei_sparse_prefill_attn(const uint16_t* q, const uint16_t* k, const uint16_t* v,

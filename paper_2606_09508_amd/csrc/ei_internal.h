@@ -136,6 +136,20 @@ bool select_supported(const SelectShape& s);
 hipError_t launch_select(const float* log_scores, const float* entropy, const SelectShape& s,
                          uint8_t* rigid, int32_t* budget_blocks, int32_t* block_idx,
                          int32_t* block_cnt, hipStream_t stream);
+// Classification and budgets only (the first kernel of launch_select).
+hipError_t launch_budget(const float* entropy, const SelectShape& s, uint8_t* rigid,
+                         int32_t* budget_blocks, hipStream_t stream);
+
+// Fused probe -> select (Algorithms 1-3 and the top-k, without ln A in
+// memory): workspace of probe_select_workspace_bytes (the probe's records
+// plus 64 bytes per (b, h, s)); supported while every past-block row fits the
+// LDS rows of the second scores kernel ((C_S - 1) r <= 2048).
+size_t probe_select_workspace_bytes(const ProbeShape& s);
+bool probe_select_supported(const ProbeShape& s);
+hipError_t launch_probe_select(const uint16_t* q, const uint16_t* k, const ProbeShape& s,
+                               double probe_scale, const SelectShape& ss, float* entropy,
+                               uint8_t* rigid, int32_t* budget_blocks, int32_t* block_idx,
+                               int32_t* block_cnt, void* workspace, hipStream_t stream);
 
 struct AttnShape {
   int B, Hq, Hkv, N, Ls, Lb, CS, CB, kmax;

@@ -42,6 +42,7 @@
 //                log1p(-(d_a + d_b)/2) with d = 1 - S[argmax] = rest/(1+rest),
 //                which keeps the tiny entropies of near one-hot rows exact.
 #include "ei_internal.h"
+#include "ei_topk.h"
 
 #include <math.h>
 
@@ -83,8 +84,19 @@ static_assert(sizeof(QMeta) == 16 && sizeof(KMeta) == 32, "record sizes");
 constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
+// Pass 1's merged softmax statistics of one (b, h, s) unit, kept by the
+// fused probe -> select path between its two kernels.
+struct UnitStats {
+  double m[2][2];     // maximum logit per (query vector a, key vector b)
+  float lse2[2][2];   // log2 (1 + rest): rest = sum of 2^(c2 (x - m)) over the other entries
+  float ltop2[2];     // log2 of the pair average at the pair's common argmax
+  int jtop[2];        // that common argmax, or -1
+};
+static_assert(sizeof(UnitStats) == 64, "record size");
+
 struct Layout {   // byte offsets of the probe records inside the workspace
   size_t qlimb, qcorr, qmeta, klimb, kmeta, kcorr, total;
+  size_t stats, total_fused;   // fused probe -> select: UnitStats per unit after the rest
 };
 Layout layout(const ProbeShape& s) {
   const size_t nq = (size_t)s.B * s.Hq * s.CS * 2;   // query vectors
@@ -98,6 +110,8 @@ Layout layout(const ProbeShape& s) {
   L.kmeta = o; o = align_up(o + nkt * kKMetaTile);
   L.kcorr = o; o = align_up(o + nkt * kKCorrTile);
   L.total = o;
+  L.stats = o; o = align_up(o + (size_t)s.B * s.Hq * s.CS * sizeof(UnitStats));
+  L.total_fused = o;
   return L;
 }
 
@@ -308,9 +322,21 @@ constexpr int kThreads = 256;                       // 4 waves
 // per wave share each staged key tile over twice the rows but need ~190
 // VGPRs (2 waves per SIMD against 4): 5% slower on the 128k layer.
 constexpr int KT = 1;
-constexpr int kUnits = kThreads / kWave * 4 * KT;
+constexpr int kWaves = kThreads / kWave;
+constexpr int kUnits = kWaves * 4 * KT;
 constexpr int kStageBytes = kKLimbTile + kKMetaTile;
 constexpr int kTilesPerStep = 2;    // key tiles staged per barrier
+
+// What a scores_kernel launch produces:
+//  kScoresWrite    ln A and the entropy (ei_entropy_probe);
+//  kScoresEntropy  the entropy and each unit's pass-1 statistics, no ln A
+//                  (the first kernel of the fused probe -> select);
+//  kScoresSelect   from those statistics, pass 2's ln A of the past blocks
+//                  into LDS rows, then each unit's top-k selection from LDS
+//                  (the second kernel of the fused path).  Same workgroups,
+//                  units and per-tile arithmetic as the other two, so every
+//                  ln A is bitwise the one kScoresWrite stores.
+enum ScoresMode { kScoresWrite = 0, kScoresEntropy = 1, kScoresSelect = 2 };
 
 __device__ __forceinline__ float hw_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float hw_log2(float x) { return __builtin_amdgcn_logf(x); }
@@ -337,11 +363,17 @@ __device__ __forceinline__ double limb_logit(const i32x4 (&acc)[2][2], int a, in
   return fma((double)p11, sk14, (double)x * sk);
 }
 
-__global__ __launch_bounds__(kThreads, 4) void scores_kernel(
+template <int MODE, int TPS, int SLOTS>
+__global__ __launch_bounds__(kThreads, MODE == kScoresSelect ? 1 : 4) void scores_kernel(
     const unsigned char* __restrict__ ws, Layout lay, float* __restrict__ log_scores,
     float* __restrict__ entropy, int Hq, int Hkv, int CS, int CB, int CBt, int r, int n_groups,
-    int n_chunks, double ps_abs, double sgn, float tau) {
+    int n_chunks, double ps_abs, double sgn, float tau, UnitStats* __restrict__ ustats,
+    const int32_t* __restrict__ kblocks, int32_t* __restrict__ idx, int32_t* __restrict__ cnt,
+    int kmax, int row_cap) {
+  constexpr int kTilesPerStep = TPS;
   __shared__ __attribute__((aligned(16))) unsigned char stage[2][kTilesPerStep * kStageBytes];
+  // kScoresSelect: kUnits rows of row_cap scores (dynamic LDS)
+  extern __shared__ __attribute__((aligned(16))) float rows_lds[];
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
   const int gq = lane >> 4, col = lane & 15;
@@ -354,7 +386,10 @@ __global__ __launch_bounds__(kThreads, 4) void scores_kernel(
   const int u0 = chunk * kUnits;
   const int ulast = min(u0 + kUnits - 1, U - 1);
   const int nv_max = min((ulast / G + 1) * r, CB);
-  const int nt = (nv_max + kTileBlocks - 1) / kTileBlocks;
+  // kScoresSelect visits the past blocks only (the segments' own blocks are
+  // always kept): up to the last unit's s r, possibly none
+  const int nt = MODE == kScoresSelect ? ((ulast / G) * r + kTileBlocks - 1) / kTileBlocks
+                                       : (nv_max + kTileBlocks - 1) / kTileBlocks;
 
   const QMeta* qmeta = (const QMeta*)(ws + lay.qmeta);
   const unsigned char* qlimb = ws + lay.qlimb;
@@ -516,10 +551,14 @@ __global__ __launch_bounds__(kThreads, 4) void scores_kernel(
         rest_[kt][a][bk] = 0.0f;
         bj_[kt][a][bk] = 0x7fffffff;
       }
+  // pass 1's merged statistics, as pass 2 uses them
+  float lse2[KT][2][2], ltop2[KT][2];
+  int jtop[KT][2];
 
   // tiles below nv_min are visible to every unit of the workgroup (when all
   // its units exist: a unit past the group's last has no row at all)
   const int nv_min = u0 + kUnits <= U ? min((u0 / G + 1) * r, CB) : 0;
+  if constexpr (MODE != kScoresSelect) {
   load_step(0);
   store_step(0);
   if (n_steps > 1) load_step(1);
@@ -567,8 +606,6 @@ __global__ __launch_bounds__(kThreads, 4) void scores_kernel(
 
   // merge the 16 lanes of each unit: max, lowest argmax, and the other
   // entries' weight relative to the max
-  float lse2[KT][2][2], ltop2[KT][2];
-  int jtop[KT][2];
 #pragma unroll
   for (int kt = 0; kt < KT; ++kt) {
     float dfc[2][2];
@@ -601,16 +638,54 @@ __global__ __launch_bounds__(kThreads, 4) void scores_kernel(
       jtop[kt][a] = bj_[kt][a][0] == bj_[kt][a][1] ? bj_[kt][a][0] : -1;
       ltop2[kt][a] = log1pf(-0.5f * (dfc[a][0] + dfc[a][1])) * kLog2e;
     }
+    if (MODE == kScoresEntropy && col == 0 && nv[kt] > 0) {
+      UnitStats us;
+#pragma unroll
+      for (int a = 0; a < 2; ++a) {
+#pragma unroll
+        for (int bk = 0; bk < 2; ++bk) {
+          us.m[a][bk] = m_[kt][a][bk];
+          us.lse2[a][bk] = lse2[kt][a][bk];
+        }
+        us.ltop2[a] = ltop2[kt][a];
+        us.jtop[a] = jtop[kt][a];
+      }
+      ustats[urow[kt]] = us;
+    }
+  }
+  } else {
+    // the statistics kept by the kScoresEntropy launch
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) {
+      UnitStats us{};
+      if (nv[kt] > 0) us = ustats[urow[kt]];
+#pragma unroll
+      for (int a = 0; a < 2; ++a) {
+#pragma unroll
+        for (int bk = 0; bk < 2; ++bk) {
+          m_[kt][a][bk] = us.m[a][bk];
+          lse2[kt][a][bk] = us.lse2[a][bk];
+        }
+        ltop2[kt][a] = us.ltop2[a];
+        jtop[kt][a] = us.jtop[a];
+      }
+    }
   }
 
-  // pass 2: ln A and the entropy
+  // pass 2: ln A and the entropy (kScoresSelect: ln A of the past blocks into
+  // the units' LDS rows)
+  int np[KT];   // past blocks s r of the lane's unit (0 for a missing unit)
+#pragma unroll
+  for (int kt = 0; kt < KT; ++kt) np[kt] = nv[kt] > 0 ? (int)(urow[kt] % CS) * r : 0;
   float H2[KT];
 #pragma unroll
   for (int kt = 0; kt < KT; ++kt) H2[kt] = 0.0f;
-  load_step(0);
-  store_step(0);
-  if (n_steps > 1) load_step(1);
-  __syncthreads();
+  if (n_steps > 0) {
+    load_step(0);
+    store_step(0);
+    if (n_steps > 1) load_step(1);
+    __syncthreads();
+  }
   for (int i = 0; i < n_steps; ++i) {
 #pragma unroll
   for (int k = 0; k < kTilesPerStep; ++k) {
@@ -635,14 +710,15 @@ __global__ __launch_bounds__(kThreads, 4) void scores_kernel(
         l2[a] = j == jtop[kt][a] ? ltop2[kt][a] : lp;
       }
       const float L2 = l2[0] > l2[1] ? l2[0] : l2[1];
-      const float h = hw_exp2(L2) * L2;
-      float* dst = log_scores + urow[kt] * CB + j;
-      if (whole) {
-        *dst = L2 * kLn2;
-        H2[kt] += h;
-      } else if (j < nv[kt]) {
-        *dst = L2 * kLn2;
-        H2[kt] += h;
+      if constexpr (MODE == kScoresSelect) {
+        if (j < np[kt]) rows_lds[(4 * KT * wave + 4 * kt + gq) * row_cap + j] = L2 * kLn2;
+      } else {
+        const float h = hw_exp2(L2) * L2;
+        float* dst = log_scores + urow[kt] * CB + j;
+        if (whole || j < nv[kt]) {
+          if constexpr (MODE == kScoresWrite) *dst = L2 * kLn2;
+          H2[kt] += h;
+        }
       }
     }
   }
@@ -652,20 +728,83 @@ __global__ __launch_bounds__(kThreads, 4) void scores_kernel(
     }
     __syncthreads();
   }
+  if constexpr (MODE != kScoresSelect) {
 #pragma unroll
-  for (int kt = 0; kt < KT; ++kt) {
-    const float h = row16_sum(H2[kt]);
-    if (col == 0 && nv[kt] > 0) entropy[urow[kt]] = -h * kLn2;
+    for (int kt = 0; kt < KT; ++kt) {
+      const float h = row16_sum(H2[kt]);
+      if (col == 0 && nv[kt] > 0) entropy[urow[kt]] = -h * kLn2;
+    }
+  } else {
+    // Top-k of each of the wave's units from its LDS row (written by this
+    // wave; the barrier above ordered the writes), with the stage buffers,
+    // free after that barrier, as the selection's histogram and candidates.
+    static_assert(kWaves * (topk::kHistWords + topk::kCandWords) * 4 <= sizeof(stage),
+                  "top-k scratch must fit the stage buffers");
+    const int wv = __builtin_amdgcn_readfirstlane(wave);
+    uint32_t* hist = (uint32_t*)&stage[0][0] + wv * (topk::kHistWords + topk::kCandWords);
+    uint32_t* cand = hist + topk::kHistWords;
+    for (int ul = 4 * KT * wv; ul < 4 * KT * (wv + 1); ++ul) {
+      const int u = u0 + ul;
+      if (u >= U) break;
+      const int64_t row = unit_row(u);
+      const float* rl = rows_lds + ul * row_cap;
+      topk::select_row<SLOTS>([&](int jj) { return rl[jj]; }, u / G, r, CB, kmax, kblocks[row],
+                              idx + row * (int64_t)kmax, cnt + row, hist, cand, lane);
+    }
   }
 }
 
 }  // namespace
 
 size_t probe_workspace_bytes(const ProbeShape& s) { return layout(s).total; }
+size_t probe_select_workspace_bytes(const ProbeShape& s) { return layout(s).total_fused; }
 
 bool probe_supported(const ProbeShape& s) {
   (void)s;
   return true;
+}
+
+namespace {
+
+// The fused path's LDS rows hold the past blocks of kUnits units: row_cap
+// floats each, a multiple of 64 plus 16 so that the four units of a wave
+// write disjoint banks.
+constexpr int kFusedMaxPast = 32 * kWave;    // the 32-slot selector's longest row
+int fused_row_cap(const ProbeShape& s) { return ((s.CS - 1) * s.r + 63) / 64 * 64 + 16; }
+size_t fused_lds_bytes(const ProbeShape& s) { return (size_t)kUnits * fused_row_cap(s) * 4; }
+constexpr size_t kLdsBytes = 160 * 1024;
+constexpr size_t kFusedStaticLds = 2 * kStageBytes;   // stage buffers of the TPS = 1 instance
+
+hipError_t launch_pool(const uint16_t* q, const uint16_t* k, const ProbeShape& s, double sgn,
+                       unsigned char* ws, const Layout& lay, int CBt, hipStream_t stream) {
+  const int64_t items = (int64_t)s.B * s.Hq * s.CS + (int64_t)s.B * s.Hkv * CBt * kTileBlocks;
+  const int64_t grid = (items + kPoolWaves - 1) / kPoolWaves;
+  hipLaunchKernelGGL(pool_kernel, dim3((unsigned)grid), dim3(kPoolThreads), 0, stream, q, k, s.B,
+                     s.Hq, s.Hkv, s.N, s.Ls, s.Lb, s.CS, s.CB, CBt, sgn, ws, lay);
+  return hipGetLastError();
+}
+
+template <int SLOTS>
+hipError_t launch_fused_select(const ProbeShape& s, const Layout& lay, unsigned char* ws,
+                               int CBt, int n_groups, int n_chunks, double ps_abs, double sgn,
+                               float tau, const int32_t* kblocks, int32_t* idx, int32_t* cnt,
+                               int kmax, hipStream_t stream) {
+  auto kern = scores_kernel<kScoresSelect, 1, SLOTS>;
+  const size_t lds = fused_lds_bytes(s);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3((unsigned)((int64_t)n_groups * n_chunks)), dim3(kThreads), lds,
+                     stream, ws, lay, nullptr, nullptr, s.Hq, s.Hkv, s.CS, s.CB, CBt, s.r,
+                     n_groups, n_chunks, ps_abs, sgn, tau, (UnitStats*)(ws + lay.stats), kblocks,
+                     idx, cnt, kmax, fused_row_cap(s));
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool probe_select_supported(const ProbeShape& s) {
+  return (s.CS - 1) * s.r <= kFusedMaxPast && fused_lds_bytes(s) + kFusedStaticLds <= kLdsBytes;
 }
 
 hipError_t launch_probe(const uint16_t* q, const uint16_t* k, const ProbeShape& s,
@@ -675,24 +814,51 @@ hipError_t launch_probe(const uint16_t* q, const uint16_t* k, const ProbeShape& 
   unsigned char* ws = (unsigned char*)workspace;
   const int CBt = (s.CB + kTileBlocks - 1) / kTileBlocks;
   const double sgn = probe_scale > 0.0 ? 1.0 : (probe_scale < 0.0 ? -1.0 : 0.0);
-  {
-    const int64_t items = (int64_t)s.B * s.Hq * s.CS + (int64_t)s.B * s.Hkv * CBt * kTileBlocks;
-    const int64_t grid = (items + kPoolWaves - 1) / kPoolWaves;
-    hipLaunchKernelGGL(pool_kernel, dim3((unsigned)grid), dim3(kPoolThreads), 0, stream, q, k,
-                       s.B, s.Hq, s.Hkv, s.N, s.Ls, s.Lb, s.CS, s.CB, CBt, sgn, ws, lay);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
+  hipError_t e = launch_pool(q, k, s, sgn, ws, lay, CBt, stream);
+  if (e != hipSuccess) return e;
   const int G = s.Hq / s.Hkv;
   const int n_groups = s.B * s.Hkv;
   const int n_chunks = (G * s.CS + kUnits - 1) / kUnits;
   const double ps_abs = fabs(probe_scale);
   // skip the residual MFMA where it moves no logit by 2^-30 or more
   const float tau = probe_scale == 0.0 ? INFINITY : (float)(0x1p-30 / ps_abs);
-  hipLaunchKernelGGL(scores_kernel, dim3((unsigned)((int64_t)n_groups * n_chunks)),
-                     dim3(kThreads), 0, stream, ws, lay, log_scores, entropy, s.Hq, s.Hkv, s.CS,
-                     s.CB, CBt, s.r, n_groups, n_chunks, ps_abs, sgn, tau);
+  hipLaunchKernelGGL((scores_kernel<kScoresWrite, kTilesPerStep, 1>),
+                     dim3((unsigned)((int64_t)n_groups * n_chunks)), dim3(kThreads), 0, stream,
+                     ws, lay, log_scores, entropy, s.Hq, s.Hkv, s.CS, s.CB, CBt, s.r, n_groups,
+                     n_chunks, ps_abs, sgn, tau, nullptr, nullptr, nullptr, nullptr, 0, 0);
   return hipGetLastError();
+}
+
+hipError_t launch_probe_select(const uint16_t* q, const uint16_t* k, const ProbeShape& s,
+                               double probe_scale, const SelectShape& ss, float* entropy,
+                               uint8_t* rigid, int32_t* budget_blocks, int32_t* block_idx,
+                               int32_t* block_cnt, void* workspace, hipStream_t stream) {
+  const Layout lay = layout(s);
+  unsigned char* ws = (unsigned char*)workspace;
+  const int CBt = (s.CB + kTileBlocks - 1) / kTileBlocks;
+  const double sgn = probe_scale > 0.0 ? 1.0 : (probe_scale < 0.0 ? -1.0 : 0.0);
+  hipError_t e = launch_pool(q, k, s, sgn, ws, lay, CBt, stream);
+  if (e != hipSuccess) return e;
+  const int G = s.Hq / s.Hkv;
+  const int n_groups = s.B * s.Hkv;
+  const int n_chunks = (G * s.CS + kUnits - 1) / kUnits;
+  const double ps_abs = fabs(probe_scale);
+  const float tau = probe_scale == 0.0 ? INFINITY : (float)(0x1p-30 / ps_abs);
+  // entropies and each unit's statistics, no ln A
+  hipLaunchKernelGGL((scores_kernel<kScoresEntropy, kTilesPerStep, 1>),
+                     dim3((unsigned)((int64_t)n_groups * n_chunks)), dim3(kThreads), 0, stream,
+                     ws, lay, nullptr, entropy, s.Hq, s.Hkv, s.CS, s.CB, CBt, s.r, n_groups,
+                     n_chunks, ps_abs, sgn, tau, (UnitStats*)(ws + lay.stats), nullptr, nullptr,
+                     nullptr, 0, 0);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  // classification and budgets (Algorithm 3) from the entropies
+  if ((e = launch_budget(entropy, ss, rigid, budget_blocks, stream)) != hipSuccess) return e;
+  // ln A again, into LDS, and the top-k from there
+  if ((s.CS - 1) * s.r <= 8 * kWave)
+    return launch_fused_select<8>(s, lay, ws, CBt, n_groups, n_chunks, ps_abs, sgn, tau,
+                                  budget_blocks, block_idx, block_cnt, ss.kmax, stream);
+  return launch_fused_select<32>(s, lay, ws, CBt, n_groups, n_chunks, ps_abs, sgn, tau,
+                                 budget_blocks, block_idx, block_cnt, ss.kmax, stream);
 }
 
 }  // namespace ei

@@ -53,6 +53,7 @@ int main() {
     for (const ei_tiling& tl : tilings) {
       sink += (size_t)ei_num_segments(d, tl) + (size_t)ei_num_blocks(d, tl);
       sink += ei_probe_workspace_bytes(d, tl) + ei_prefill_workspace_bytes(d, tl);
+      sink += ei_probe_select_workspace_bytes(d, tl);
       for (const ei_budget_params& pp : params) sink += (size_t)ei_kmax(tl, pp);
     }
   std::printf("helpers swept (%zu)\n", sink % 7);
@@ -79,6 +80,28 @@ int main() {
       EXPECT(ei_select_blocks(FF, FF, d, t, pp, km, FU, FI, FI, FI, nullptr) < 0);
   for (int mode : {-1, 3, INT_MAX})
     EXPECT(ei_select_blocks_mode(FF, FF, d, t, p, mode, km, FU, FI, FI, FI, nullptr) < 0);
+  // fused probe -> select
+  const size_t fws = ei_probe_select_workspace_bytes(d, t);
+  EXPECT(fws > ws);
+  EXPECT(ei_probe_select_fused(F16, F16, d, t, 1.0, p, 0, km, FF, FU, FI, FI, FI, FV, fws - 1,
+                               nullptr) == EI_ERR_WORKSPACE);
+  EXPECT(ei_probe_select_fused(F16, nullptr, d, t, 1.0, p, 0, km, FF, FU, FI, FI, FI, FV, fws,
+                               nullptr) == EI_ERR_NULL);
+  EXPECT(ei_probe_select_fused(F16, F16, d, t, 1.0, p, 3, km, FF, FU, FI, FI, FI, FV, fws,
+                               nullptr) == EI_ERR_SHAPE);
+  EXPECT(ei_probe_select_fused(F16, F16, d, t, NAN, p, 0, km, FF, FU, FI, FI, FI, FV, fws,
+                               nullptr) == EI_ERR_SHAPE);
+  EXPECT(ei_probe_select_fused(F16, F16, d, t, 1.0, p, 0, km - 1, FF, FU, FI, FI, FI, FV, fws,
+                               nullptr) == EI_ERR_SHAPE);
+  {
+    const ei_dims longer{1, 4, 1, 131072 + 129, 128};   // 2050 past blocks in the last segment
+    EXPECT(ei_probe_select_fused(F16, F16, longer, t, 1.0, p, 0, km, FF, FU, FI, FI, FI, FV,
+                                 ei_probe_select_workspace_bytes(longer, t),
+                                 nullptr) == EI_ERR_UNSUPPORTED);
+  }
+  for (const ei_dims& dd : huge)
+    EXPECT(ei_probe_select_fused(F16, F16, dd, t, 1.0, p, 0, km, FF, FU, FI, FI, FI, FV, fws,
+                                 nullptr) < 0);
   // attention
   EXPECT(ei_sparse_prefill_attn(F16, F16, F16, d, t, NAN, FI, FI, km, F16, nullptr) ==
          EI_ERR_SHAPE);

@@ -35,7 +35,7 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_helpers(L):
-    assert L.ei_abi_version() == 5
+    assert L.ei_abi_version() == 6
     assert eb.kmax(128, 64, 2048, 3) == 98
     assert eb.kmax(2048, 64, 2048, 3) == 96 + 32
     assert eb.kmax(256, 128, 256, 3) == 6 + 2
@@ -350,3 +350,41 @@ def test_ragged_sequence_lengths_are_accepted(L, n, tiling):
     km = L.ei_kmax(t, p)
     assert L.ei_entropy_guided_prefill(FAKE, FAKE, FAKE, d, t, 1.0, p, 0, km, 0.088,
                                        *((FAKE,) * 7), FAKE, 0, None) == -4
+
+
+def test_fused_probe_select_refusals(L):
+    """ei_probe_select_fused validates like the probe and the selection
+    together, needs the probe workspace plus 64 bytes per (b, h, s), and
+    refuses rows of more than 2048 past blocks (its LDS rows), all before
+    anything is launched."""
+    t, p = eb.Tiling(128, 64), eb.budget_params()
+    km = L.ei_kmax(t, p)
+    call = L.ei_probe_select_fused
+    outs = (FAKE,) * 5
+    for n in (1024, 131072):
+        d = eb.Dims(2, 32, 8, n, 128)
+        need = L.ei_probe_select_workspace_bytes(d, t)
+        assert need >= L.ei_probe_workspace_bytes(d, t) + 2 * 32 * (n // 128) * 64
+        assert call(FAKE, FAKE, d, t, 1.0, p, 0, km, *outs, FAKE, need - 1, None) == -4
+        assert call(FAKE, FAKE, d, t, 1.0, p, 0, km, *outs, None, need, None) == -4
+    d = eb.Dims(1, 4, 1, 1024, 128)
+    need = L.ei_probe_select_workspace_bytes(d, t)
+    assert call(None, FAKE, d, t, 1.0, p, 0, km, *outs, FAKE, need, None) == -1
+    assert call(FAKE, FAKE, d, t, 1.0, p, 0, km, FAKE, FAKE, None, FAKE, FAKE, FAKE, need,
+                None) == -1
+    assert call(FAKE, FAKE, d, t, 1.0, p, 3, km, *outs, FAKE, need, None) == -2
+    assert call(FAKE, FAKE, d, t, 1.0, p, 0, km - 1, *outs, FAKE, need, None) == -2
+    assert call(FAKE, FAKE, d, t, float("nan"), p, 0, km, *outs, FAKE, need, None) == -2
+    assert call(FAKE, FAKE, eb.Dims(1, 4, 1, 1024, 96), t, 1.0, p, 0, km, *outs, FAKE, need,
+                None) == -3
+    assert call(None, None, eb.Dims(0, 4, 1, 1024, 128), t, 1.0, p, 0, km, *(None,) * 5, None,
+                0, None) == 0
+    # the longest supported rows: 2048 past blocks (the last segment at 131072 + 128 tokens
+    # with L_S = 128, L_B = 64 has 2048; one token more starts a segment with 2050)
+    for n, tl, ok in ((131072 + 128, (128, 64), True), (131072 + 129, (128, 64), False),
+                      (262144 + 256, (256, 128), True), (262144 + 257, (256, 128), False)):
+        dd, tt = eb.Dims(1, 4, 1, n, 128), eb.Tiling(*tl)
+        kk = L.ei_kmax(tt, p)
+        need = L.ei_probe_select_workspace_bytes(dd, tt)
+        st = call(FAKE, FAKE, dd, tt, 1.0, p, 0, kk, *outs, FAKE, 0, None)
+        assert st == (-4 if ok else -3), (n, tl, st)

@@ -602,6 +602,20 @@ def test_c3_llama8b_128k(c3):
     say(f"  attn ({len(rows)} rows) max {amax:.2e} mean {amean:.2e}")
 
 
+def test_c3_fused_probe_select(c3):
+    """The fused probe -> select at the 128k layer (the longest rows it
+    supports, 2046 past blocks): bitwise the separate calls' entropies and
+    selections, which equal the oracle's selection on the GPU's ln A."""
+    w, r = c3
+    en2, sel2 = eb.probe_select_fused(r["q"], r["k"], w.Ls, w.Lb, w.e_t, w.alpha, w.delta_t,
+                                      w.base_budget, w.mult, w.probe_scale)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(en2.cpu().numpy(), r["en"])
+    for name in ("rigid", "budget", "idx", "cnt"):
+        np.testing.assert_array_equal(sel2[name].cpu().numpy(), r["sel"][name], err_msg=name)
+    say("  fused probe -> select bitwise equal to the separate calls")
+
+
 def test_c3_dense_sampled(c3):
     w, r = c3
     od = eb.dense_prefill_attn(r["q"], r["k"], r["v"], w.softmax_scale, True)
@@ -711,6 +725,58 @@ def test_one_call_prefill_equals_separate_calls(case, mode):
     for name in ("rigid", "budget", "idx", "cnt"):
         assert torch.equal(sel[name], sel2[name]), name
     assert torch.equal(o, o2)
+
+
+FUSED_CASES = [
+    (dict(), eb.CLASSIFY_HEAD),
+    (dict(N=1000), eb.CLASSIFY_HEAD),                    # ragged tail
+    (dict(N=64), eb.CLASSIFY_HEAD),                      # no past blocks anywhere
+    (dict(N=1), eb.CLASSIFY_HEAD),
+    (dict(N=200, B=3, Hq=1, Hkv=1), eb.CLASSIFY_HEAD),
+    (dict(B=2, N=640), eb.CLASSIFY_HEAD),
+    (dict(Hq=7, Hkv=1, N=512), eb.CLASSIFY_GQA_GROUP),
+    (dict(Ls=256, Lb=128, N=1280, base_budget=512), eb.CLASSIFY_SEGMENT),
+    (dict(N=2048, base_budget=0), eb.CLASSIFY_HEAD),     # own blocks only
+    (dict(N=2048, base_budget=64), eb.CLASSIFY_HEAD),    # k = 1
+    (dict(B=2, Hq=4, Hkv=2, N=16384 + 320), eb.CLASSIFY_HEAD),
+    (dict(Hq=7, Hkv=1, N=16384 + 64), eb.CLASSIFY_GQA_GROUP),
+    (dict(Hq=4, Hkv=2, Ls=256, Lb=128, N=16384 + 384, base_budget=512), eb.CLASSIFY_SEGMENT),
+    (dict(Hq=8, Hkv=2, N=40960), eb.CLASSIFY_HEAD),      # the 32-slot selector instance
+]
+
+
+def _check_fused(w, mode, ls, en, sel, en2, sel2):
+    """The fused path against the separate calls (bitwise) and against the
+    oracle's selection on the separate probe's ln A (bit-exact)."""
+    assert torch.equal(en, en2), "entropy"
+    for name in ("rigid", "budget", "idx", "cnt"):
+        assert torch.equal(sel[name], sel2[name]), name
+    ref = oracle.select(ls.cpu().numpy(), en.cpu().numpy(), w.N, w.Ls, w.Lb, w.e_t, w.alpha,
+                        w.delta_t, w.base_budget, w.mult, mode=mode, n_kv_heads=w.Hkv)
+    for name in ("rigid", "budget", "cnt", "idx"):
+        np.testing.assert_array_equal(sel2[name].cpu().numpy(), ref[name], err_msg=name)
+
+
+@pytest.mark.parametrize("case,mode", FUSED_CASES,
+                         ids=lambda c: ",".join(f"{k}={v}" for k, v in c.items())
+                         if isinstance(c, dict) else str(c))
+def test_fused_probe_select_equals_separate_calls(case, mode):
+    """ei_probe_select_fused (ln A never in memory) gives bitwise the
+    entropies and selections of ei_entropy_probe + ei_select_blocks_mode, and
+    they equal the oracle's selection on that ln A."""
+    w = synth.make("c1", 9, **case)
+    say(f"[fused] {case} mode={mode}")
+    q, k = to_dev(w.q), to_dev(w.k)
+    ls, en = eb.entropy_probe(q, k, w.Ls, w.Lb, w.probe_scale)
+    sel = eb.select_blocks(ls, en, w.N, w.Ls, w.Lb, w.e_t, w.alpha, w.delta_t, w.base_budget,
+                           w.mult, n_kv_heads=w.Hkv, mode=mode)
+    bufs = {}
+    for _ in range(2):   # a second call into the same buffers and workspace
+        en2, sel2 = eb.probe_select_fused(q, k, w.Ls, w.Lb, w.e_t, w.alpha, w.delta_t,
+                                          w.base_budget, w.mult, w.probe_scale, mode=mode,
+                                          bufs=bufs)
+        torch.cuda.synchronize()
+        _check_fused(w, mode, ls, en, sel, en2, sel2)
 
 
 def test_one_call_prefill_c2_repeated():

@@ -35,6 +35,8 @@ def test_bench_line_contract():
     assert rf["bound"] == "mfma" and rf["unit"] == "TFLOP/s" and rf["peak"] == 2500.0
     assert 0 < rf["achieved"] and abs(rf["frac"] - rf["achieved"] / rf["peak"]) < 1e-3
     assert rf["traffic"] is None and d["mfma_busy_counter"] is None
+    pf = d["probe_select_fused"]
+    assert pf["bitwise_equal_to_separate"] is True and pf["ms"] > 0
     cb = d["cpu_baseline"]
     assert cb["kind"] == "oracle" and cb["value"] > 0 and cb["cores"] >= 1
     assert cb["unit"] == "ms/layer" and cb["sample"]
