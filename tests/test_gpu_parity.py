@@ -602,11 +602,10 @@ def test_c3_llama8b_128k(c3):
     say(f"  attn ({len(rows)} rows) max {amax:.2e} mean {amean:.2e}")
 
 
-def test_c3_fused_probe_select(c3):
-    """The fused probe -> select at the 128k layer (the longest rows it
-    supports, 2046 past blocks): bitwise the separate calls' entropies and
-    selections, which equal the oracle's selection on the GPU's ln A."""
-    w, r = c3
+def _fused_equals_path(w, r):
+    """ei_probe_select_fused on a workload's inputs: bitwise the entropies and
+    selections of the separate calls in r (which check_select holds to the
+    oracle's selection on the same ln A)."""
     en2, sel2 = eb.probe_select_fused(r["q"], r["k"], w.Ls, w.Lb, w.e_t, w.alpha, w.delta_t,
                                       w.base_budget, w.mult, w.probe_scale)
     torch.cuda.synchronize()
@@ -614,6 +613,13 @@ def test_c3_fused_probe_select(c3):
     for name in ("rigid", "budget", "idx", "cnt"):
         np.testing.assert_array_equal(sel2[name].cpu().numpy(), r["sel"][name], err_msg=name)
     say("  fused probe -> select bitwise equal to the separate calls")
+
+
+def test_c3_fused_probe_select(c3):
+    """The fused probe -> select at the 128k layer (the longest rows it
+    supports, 2046 past blocks)."""
+    w, r = c3
+    _fused_equals_path(w, r)
 
 
 def test_c3_dense_sampled(c3):
@@ -647,6 +653,7 @@ def test_c4_qwen7b_64k_sampled():
     assert span_blocks and ((rec >= 0) & (rec <= 1)).all()
     say(f"  span-block recall in the last segment: mean {rec.mean():.3f}, min {rec.min():.3f} "
         f"over {w.B * w.Hq} heads ({len(span_blocks)} span blocks)")
+    _fused_equals_path(w, r)   # G = 7, residual-heavy probe tiles
 
 
 def test_c5_llama70b_128k_sampled():
@@ -678,6 +685,7 @@ def test_c5_llama70b_128k_sampled():
         del ls, en, sel
     amax, amean = check_attention(w, r, _sample_query_rows(w, n=32, seed=6))
     say(f"  entropy rel {hrel:.2e} L {lerr:.2e} attn {amax:.2e}/{amean:.2e}")
+    _fused_equals_path(w, r)
 
 
 def test_maximum_block_count():
