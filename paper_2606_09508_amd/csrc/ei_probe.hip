@@ -19,11 +19,13 @@
 // the logits equal the plain binary64 definition up to its own rounding.
 //
 // Two kernels:
-//  pool_kernel   streams Q and K once from HBM (the bound of the probe),
-//                pools each L_S-row query segment and L_B-row key block to
-//                its max / min vectors and writes their limbs, residual
-//                parts and scales: query records per vector, key records
-//                tiled by 16 blocks in the order the MFMA operands are read.
+//  pool_kernel   streams K once from HBM, pools each L_B-row key block to its
+//                max / min vectors and writes their limbs, residual parts and
+//                scales, tiled by 16 blocks in the order the MFMA operands
+//                are read.  The same code (pool_item) pools each L_S-row
+//                query segment into per-vector records, run by the scores
+//                kernel for its own units, so that the stream of Q (the
+//                probe's largest read) overlaps the logits.
 //  scores_kernel one workgroup of 4 waves per (batch, KV head, 16 query
 //                units), a unit being one (query head, segment) of the KV
 //                group, segment-major.  Each wave owns 4 units as one
@@ -200,14 +202,12 @@ __device__ __forceinline__ Split split_vector(const float* x) {
 // zeros).  Lanes c = lane % 16 hold dims 8c .. 8c+7 of rows of phase
 // lane / 16; after the reduction lanes 0-15 split the max vector and lanes
 // 16-31 the min vector.
-__global__ __launch_bounds__(kPoolThreads) void pool_kernel(
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, int B, int Hq, int Hkv,
-    int N, int Ls, int Lb, int CS, int CB, int CBt, double sgn, unsigned char* __restrict__ ws,
-    Layout lay) {
-  const int lane = threadIdx.x & (kWave - 1);
-  const int64_t item = (int64_t)blockIdx.x * kPoolWaves + (threadIdx.x >> 6);
-  const int64_t nq = (int64_t)B * Hq * CS, nk = (int64_t)B * Hkv * CBt * kTileBlocks;
-  if (item >= nq + nk) return;
+__device__ __forceinline__ void pool_item(const uint16_t* __restrict__ q,
+                                          const uint16_t* __restrict__ k, int B, int Hq, int Hkv,
+                                          int N, int Ls, int Lb, int CS, int CB, int CBt,
+                                          double sgn, unsigned char* __restrict__ ws,
+                                          const Layout& lay, int64_t item, int lane) {
+  const int64_t nq = (int64_t)B * Hq * CS;
   const bool is_q = item < nq;
   const int64_t head = is_q ? item / CS : (item - nq) / ((int64_t)CBt * kTileBlocks);
   const int grp = (int)(is_q ? item % CS : (item - nq) % ((int64_t)CBt * kTileBlocks));
@@ -224,13 +224,15 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kernel(
     const int rows = (int)min((int64_t)L, (int64_t)N - row0);
     const uint16_t* base = (is_q ? q : k) + ((size_t)head * N + row0) * kHeadDim;
     int r = ph;
-    for (; r + 12 < rows; r += 16) {
-      uint4 w[4];
+    // 64 rows (16 loads of 16 bytes per lane) in flight at a time: a query
+    // segment of 128 rows takes two round trips to HBM, a key block one
+    for (; r + 60 < rows; r += 64) {
+      uint4 w[16];
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < 16; ++u)
         w[u] = *(const uint4*)(base + (size_t)(r + 4 * u) * kHeadDim + 8 * c);
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < 16; ++u) {
         const uint32_t ww[4] = {w[u].x, w[u].y, w[u].z, w[u].w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -313,6 +315,21 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kernel(
   }
 }
 
+// One wave per item: a query segment (B*Hq*C_S items, the first) or a key
+// block slot (B*Hkv*C_Bt*16 items); item_offset selects where the launch
+// starts (the scores kernel pools the query segments it uses itself).
+__global__ __launch_bounds__(kPoolThreads) void pool_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, int B, int Hq, int Hkv,
+    int N, int Ls, int Lb, int CS, int CB, int CBt, double sgn, unsigned char* __restrict__ ws,
+    Layout lay, int64_t item_offset) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t item = item_offset + (int64_t)blockIdx.x * kPoolWaves + (threadIdx.x >> 6);
+  const int64_t nq = (int64_t)B * Hq * CS, nk = (int64_t)B * Hkv * CBt * kTileBlocks;
+  if (item >= nq + nk) return;
+  pool_item(q, k, B, Hq, Hkv, N, Ls, Lb, CS, CB, CBt, sgn, ws, lay, item, lane);
+}
+
+
 // ---------------------------------------------------------------------------
 // Logits, softmax statistics, ln A and the entropy
 // ---------------------------------------------------------------------------
@@ -365,7 +382,8 @@ __device__ __forceinline__ double limb_logit(const i32x4 (&acc)[2][2], int a, in
 
 template <int MODE, int TPS, int SLOTS>
 __global__ __launch_bounds__(kThreads, MODE == kScoresSelect ? 1 : 4) void scores_kernel(
-    const unsigned char* __restrict__ ws, Layout lay, float* __restrict__ log_scores,
+    const uint16_t* __restrict__ qsrc, int B, int N, int Ls, int Lb,
+    unsigned char* __restrict__ ws, Layout lay, float* __restrict__ log_scores,
     float* __restrict__ entropy, int Hq, int Hkv, int CS, int CB, int CBt, int r, int n_groups,
     int n_chunks, double ps_abs, double sgn, float tau, UnitStats* __restrict__ ustats,
     const int32_t* __restrict__ kblocks, int32_t* __restrict__ idx, int32_t* __restrict__ cnt,
@@ -402,6 +420,21 @@ __global__ __launch_bounds__(kThreads, MODE == kScoresSelect ? 1 : 4) void score
     const int s = u / G, hh = u % G;
     return ((int64_t)(b * Hq + g * G + hh)) * CS + s;
   };
+
+  // The query segments of the workgroup's own units are pooled here (only
+  // this workgroup reads their records, after the barrier), so that their
+  // HBM reads overlap the logits of the CU's other workgroups; the key blocks
+  // are pooled beforehand by pool_kernel.  kScoresSelect reads the records
+  // its kScoresEntropy launch wrote.
+  if constexpr (MODE != kScoresSelect) {
+    for (int t = 0; t < 4 * KT; ++t) {
+      const int u = u0 + 4 * KT * wave + t;
+      if (u < U)
+        pool_item(qsrc, nullptr, B, Hq, Hkv, N, Ls, Lb, CS, CB, CBt, sgn, ws, lay, unit_row(u),
+                  lane);
+    }
+    __syncthreads();
+  }
 
   // This lane's units (D rows 4 gq .. 4 gq + 3 of each tile): row, visible
   // blocks (0 for a unit past the group's last), per query vector a the
@@ -775,12 +808,14 @@ size_t fused_lds_bytes(const ProbeShape& s) { return (size_t)kUnits * fused_row_
 constexpr size_t kLdsBytes = 160 * 1024;
 constexpr size_t kFusedStaticLds = 2 * kStageBytes;   // stage buffers of the TPS = 1 instance
 
+// The key blocks only (the scores kernels pool the query segments).
 hipError_t launch_pool(const uint16_t* q, const uint16_t* k, const ProbeShape& s, double sgn,
                        unsigned char* ws, const Layout& lay, int CBt, hipStream_t stream) {
-  const int64_t items = (int64_t)s.B * s.Hq * s.CS + (int64_t)s.B * s.Hkv * CBt * kTileBlocks;
+  const int64_t nq = (int64_t)s.B * s.Hq * s.CS;
+  const int64_t items = (int64_t)s.B * s.Hkv * CBt * kTileBlocks;
   const int64_t grid = (items + kPoolWaves - 1) / kPoolWaves;
   hipLaunchKernelGGL(pool_kernel, dim3((unsigned)grid), dim3(kPoolThreads), 0, stream, q, k, s.B,
-                     s.Hq, s.Hkv, s.N, s.Ls, s.Lb, s.CS, s.CB, CBt, sgn, ws, lay);
+                     s.Hq, s.Hkv, s.N, s.Ls, s.Lb, s.CS, s.CB, CBt, sgn, ws, lay, nq);
   return hipGetLastError();
 }
 
@@ -795,7 +830,8 @@ hipError_t launch_fused_select(const ProbeShape& s, const Layout& lay, unsigned 
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, dim3((unsigned)((int64_t)n_groups * n_chunks)), dim3(kThreads), lds,
-                     stream, ws, lay, nullptr, nullptr, s.Hq, s.Hkv, s.CS, s.CB, CBt, s.r,
+                     stream, nullptr, s.B, s.N, s.Ls, s.Lb, ws, lay, nullptr, nullptr, s.Hq, s.Hkv,
+                     s.CS, s.CB, CBt, s.r,
                      n_groups, n_chunks, ps_abs, sgn, tau, (UnitStats*)(ws + lay.stats), kblocks,
                      idx, cnt, kmax, fused_row_cap(s));
   return hipGetLastError();
@@ -824,7 +860,8 @@ hipError_t launch_probe(const uint16_t* q, const uint16_t* k, const ProbeShape& 
   const float tau = probe_scale == 0.0 ? INFINITY : (float)(0x1p-30 / ps_abs);
   hipLaunchKernelGGL((scores_kernel<kScoresWrite, kTilesPerStep, 1>),
                      dim3((unsigned)((int64_t)n_groups * n_chunks)), dim3(kThreads), 0, stream,
-                     ws, lay, log_scores, entropy, s.Hq, s.Hkv, s.CS, s.CB, CBt, s.r, n_groups,
+                     q, s.B, s.N, s.Ls, s.Lb, ws, lay, log_scores, entropy, s.Hq, s.Hkv, s.CS,
+                     s.CB, CBt, s.r, n_groups,
                      n_chunks, ps_abs, sgn, tau, nullptr, nullptr, nullptr, nullptr, 0, 0);
   return hipGetLastError();
 }
@@ -847,7 +884,8 @@ hipError_t launch_probe_select(const uint16_t* q, const uint16_t* k, const Probe
   // entropies and each unit's statistics, no ln A
   hipLaunchKernelGGL((scores_kernel<kScoresEntropy, kTilesPerStep, 1>),
                      dim3((unsigned)((int64_t)n_groups * n_chunks)), dim3(kThreads), 0, stream,
-                     ws, lay, nullptr, entropy, s.Hq, s.Hkv, s.CS, s.CB, CBt, s.r, n_groups,
+                     q, s.B, s.N, s.Ls, s.Lb, ws, lay, nullptr, entropy, s.Hq, s.Hkv, s.CS,
+                     s.CB, CBt, s.r, n_groups,
                      n_chunks, ps_abs, sgn, tau, (UnitStats*)(ws + lay.stats), nullptr, nullptr,
                      nullptr, 0, 0);
   if ((e = hipGetLastError()) != hipSuccess) return e;
