@@ -197,6 +197,93 @@ __device__ __forceinline__ Split split_vector(const float* x) {
   return o;
 }
 
+// The records of query segment `item` from its pooled max (lanes 0-15) or
+// min (lanes 16-31) vector: limbs, [q_r | q_g] and the scale record.
+__device__ __forceinline__ void store_query(const float* x, int64_t item,
+                                           unsigned char* __restrict__ ws, const Layout& lay,
+                                           int lane) {
+  const int c = lane & 15, m = lane >> 4;
+  const Split sp = split_vector(x);
+  const size_t v = (size_t)item * 2 + m;   // query vector index
+  unsigned char* ql = ws + lay.qlimb + v * kQLimb;
+  *(uint2*)(ql + 8 * c) = make_uint2(sp.lo[0], sp.lo[1]);
+  *(uint2*)(ql + kHeadDim + 8 * c) = make_uint2(sp.hi[0], sp.hi[1]);
+  uint16_t* qc = (uint16_t*)(ws + lay.qcorr) + v * kQCorr;
+  *(uint4*)(qc + 8 * c) = make_uint4(sp.xr[0], sp.xr[1], sp.xr[2], sp.xr[3]);
+  *(uint4*)(qc + kHeadDim + 8 * c) = make_uint4(sp.xg[0], sp.xg[1], sp.xg[2], sp.xg[3]);
+  if (c == 0)
+    ((QMeta*)(ws + lay.qmeta))[v] =
+        QMeta{sp.nonfinite ? (double)NAN : ldexp(1.0, sp.F), sp.R, sp.A};
+}
+
+// Folds BL rows (BL chunks of 16 bytes a lane) into the lane's max / min.
+template <int BL>
+__device__ __forceinline__ void fold_rows(const uint4 (&w)[BL], float (&mx)[8], float (&mn)[8]) {
+#pragma unroll
+  for (int u = 0; u < BL; ++u) {
+    const uint32_t ww[4] = {w[u].x, w[u].y, w[u].z, w[u].w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float lo = bf16_lo(ww[e]), hi = bf16_hi(ww[e]);
+      mx[2 * e] = fmaxf(mx[2 * e], lo);
+      mn[2 * e] = fminf(mn[2 * e], lo);
+      mx[2 * e + 1] = fmaxf(mx[2 * e + 1], hi);
+      mn[2 * e + 1] = fminf(mn[2 * e + 1], hi);
+    }
+  }
+}
+
+// Four whole query segments (items it[0..3], each L_S = 128 rows, so 32 rows
+// a lane) pooled by one wave as one stream of batches of BL loads a lane, NB
+// batches in flight (a batch's slot is refilled as soon as it is folded), so
+// the stream runs on across segment boundaries; a segment is split and
+// written as soon as its last batch is folded.  The segment bases are
+// wave-uniform (scalar registers).  Against one segment at a time (two
+// round trips of 16 loads each): 1-3% faster probe, same records.
+constexpr int kQBatch = 4, kQRing = 4;
+__device__ __forceinline__ void pool_query4(const uint16_t* __restrict__ q, int N,
+                                            const int64_t (&it)[4], int CS,
+                                            unsigned char* __restrict__ ws, const Layout& lay,
+                                            int lane) {
+  constexpr int BL = kQBatch, NB = kQRing, PER = 32 / BL, NBAT = 4 * PER;
+  const int c = lane & 15, ph = lane >> 4;
+  const uint32_t loff = (uint32_t)(ph * kHeadDim + 8 * c) * 2u;   // bytes
+  const unsigned char* base[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+    base[t] = (const unsigned char*)(q + ((size_t)(it[t] / CS) * N + (size_t)(it[t] % CS) * 128) *
+                                             kHeadDim);
+  uint4 w[NB][BL];
+  auto issue = [&](int b) {
+#pragma unroll
+    for (int i = 0; i < BL; ++i)
+      w[b % NB][i] = *(const uint4*)(base[b / PER] + loff +
+                                     (uint32_t)(4 * (BL * (b % PER) + i)) * (kHeadDim * 2u));
+  };
+  float mx[8], mn[8];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) issue(b);
+#pragma unroll
+  for (int b = 0; b < NBAT; ++b) {
+    if (b % PER == 0) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) { mx[e] = -INFINITY; mn[e] = INFINITY; }
+    }
+    fold_rows<BL>(w[b % NB], mx, mn);
+    if (b + NB < NBAT) issue(b + NB);   // into the slot just folded
+    if (b % PER == PER - 1) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        mx[e] = fmaxf(mx[e], __shfl_xor(mx[e], 16));
+        mx[e] = fmaxf(mx[e], __shfl_xor(mx[e], 32));
+        mn[e] = fminf(mn[e], __shfl_xor(mn[e], 16));
+        mn[e] = fminf(mn[e], __shfl_xor(mn[e], 32));
+      }
+      if (ph < 2) store_query(ph == 0 ? mx : mn, it[b / PER], ws, lay, lane);
+    }
+  }
+}
+
 // One wave per item: a query segment (B*Hq*C_S items) or a key block slot
 // (B*Hkv*C_Bt*16 items, C_Bt = ceil(C_B / 16); slots past C_B are written as
 // zeros).  Lanes c = lane % 16 hold dims 8c .. 8c+7 of rows of phase
@@ -268,23 +355,15 @@ __device__ __forceinline__ void pool_item(const uint16_t* __restrict__ q,
     for (int e = 0; e < 8; ++e) { mx[e] = 0.0f; mn[e] = 0.0f; }
   }
   if (ph >= 2) return;
+  if (is_q) {
+    store_query(ph == 0 ? mx : mn, item, ws, lay, lane);
+    return;
+  }
   const int m = ph;   // 0: max vector, 1: min vector
   const Split sp = split_vector(m == 0 ? mx : mn);
   const uint2 lo = make_uint2(sp.lo[0], sp.lo[1]), hi = make_uint2(sp.hi[0], sp.hi[1]);
   const uint4 xr = make_uint4(sp.xr[0], sp.xr[1], sp.xr[2], sp.xr[3]);
-  const uint4 xg = make_uint4(sp.xg[0], sp.xg[1], sp.xg[2], sp.xg[3]);
-  if (is_q) {
-    const size_t v = (size_t)item * 2 + m;   // query vector index
-    unsigned char* ql = ws + lay.qlimb + v * kQLimb;
-    *(uint2*)(ql + 8 * c) = lo;
-    *(uint2*)(ql + kHeadDim + 8 * c) = hi;
-    uint16_t* qc = (uint16_t*)(ws + lay.qcorr) + v * kQCorr;
-    *(uint4*)(qc + 8 * c) = xr;
-    *(uint4*)(qc + kHeadDim + 8 * c) = xg;
-    if (c == 0)
-      ((QMeta*)(ws + lay.qmeta))[v] =
-          QMeta{sp.nonfinite ? (double)NAN : ldexp(1.0, sp.F), sp.R, sp.A};
-  } else {
+  {
     const int t = grp / kTileBlocks, j = grp % kTileBlocks;
     const size_t tile = (size_t)head * CBt + t;
     // limb l of dims d = 8c .. 8c+7: sub-block ((m, l), d / 64), then lane
@@ -427,11 +506,18 @@ __global__ __launch_bounds__(kThreads, MODE == kScoresSelect ? 1 : 4) void score
   // are pooled beforehand by pool_kernel.  kScoresSelect reads the records
   // its kScoresEntropy launch wrote.
   if constexpr (MODE != kScoresSelect) {
-    for (int t = 0; t < 4 * KT; ++t) {
-      const int u = u0 + 4 * KT * wave + t;
-      if (u < U)
-        pool_item(qsrc, nullptr, B, Hq, Hkv, N, Ls, Lb, CS, CB, CBt, sgn, ws, lay, unit_row(u),
-                  lane);
+    const int uw = u0 + 4 * KT * __builtin_amdgcn_readfirstlane(wave);
+    // whole segments: L_S = 128 and the wave's last unit's segment ends by N
+    if (KT == 1 && Ls == 128 && uw + 3 < U && (int64_t)((uw + 3) / G + 1) * 128 <= N) {
+      const int64_t it[4] = {unit_row(uw), unit_row(uw + 1), unit_row(uw + 2), unit_row(uw + 3)};
+      pool_query4(qsrc, N, it, CS, ws, lay, lane);
+    } else {
+      for (int t = 0; t < 4 * KT; ++t) {
+        const int u = uw + t;
+        if (u < U)
+          pool_item(qsrc, nullptr, B, Hq, Hkv, N, Ls, Lb, CS, CB, CBt, sgn, ws, lay, unit_row(u),
+                    lane);
+      }
     }
     __syncthreads();
   }
