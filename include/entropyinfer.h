@@ -37,10 +37,12 @@
  *    256-byte aligned memory); a pointer that is not returns
  *    EI_ERR_UNSUPPORTED.
  *  - Outputs must not alias inputs.  Identical inputs give bitwise-identical
- *    outputs (the only atomics are integer counts in LDS, whose order does
- *    not matter).  No global state (except the no-allocation variant's
- *    scratch array), no logging; calls on different streams may run
- *    concurrently.
+ *    outputs (the only atomics are integer counts: in LDS, and the sparse
+ *    attention's work-queue counters in its workspace, which decide which
+ *    workgroup computes a tile but not what it computes).  No global state
+ *    (except the no-allocation variant's scratch array), no logging; calls
+ *    on different streams may run concurrently when they do not share a
+ *    workspace.
  */
 #ifndef ENTROPYINFER_H
 #define ENTROPYINFER_H
@@ -255,13 +257,30 @@ ei_status ei_probe_select_fused(const uint16_t* q, const uint16_t* k, ei_dims di
  * 2^17 keys).  A sub-block in which a lane's probabilities sum past 2^32
  * (or overflow) is formed again after the row maximum is raised.
  *
+ *   workspace      NULL, or EI_ATTN_WORKSPACE_BYTES of device memory for the
+ *                  kernel's work-queue counters (zeroed on `stream` by the
+ *                  call itself; a workspace must not be shared by calls that
+ *                  may run at the same time)
+ *
+ * Scheduling (results are bitwise the same either way): with a workspace
+ * and B * Hkv a multiple or a divisor of 8, the kernel is persistent (two
+ * workgroups per CU), each XCD working through a queue of the (tile, query
+ * head) items of its own KV groups (or of its share of one group's tiles),
+ * heaviest tiles first, then taking items from the other XCDs' queues; K/V
+ * blocks then stay in the L2 of the XCD whose tiles select them.  Otherwise
+ * one workgroup per (tile, query head) on a static grid.
+ *
  * Errors: EI_ERR_NULL, EI_ERR_SHAPE (also kmax <= 0 or a softmax_scale that is
- * not finite and positive), EI_ERR_UNSUPPORTED, EI_ERR_LAUNCH.
+ * not finite and positive), EI_ERR_UNSUPPORTED (also a workspace not 16-byte
+ * aligned), EI_ERR_WORKSPACE (a workspace under EI_ATTN_WORKSPACE_BYTES),
+ * EI_ERR_LAUNCH.
  */
+#define EI_ATTN_WORKSPACE_BYTES ((size_t)256)
 ei_status ei_sparse_prefill_attn(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                                  ei_dims dims, ei_tiling tiling, float softmax_scale,
                                  const int32_t* block_idx, const int32_t* block_cnt,
-                                 int32_t kmax, uint16_t* o, void* stream);
+                                 int32_t kmax, uint16_t* o, void* workspace,
+                                 size_t workspace_bytes, void* stream);
 
 /*
  * ei_sparse_prefill_attn_gqa_union -- the same attention as
@@ -270,8 +289,8 @@ ei_status ei_sparse_prefill_attn(const uint16_t* q, const uint16_t* k, const uin
  * budgets, whose heads no longer share K/V loads): one workgroup takes a
  * query tile of two query heads of the same KV head,
  * copies each block of the union of their lists once and lets each head
- * compute only its own blocks.  Same arguments and bitwise the same output as
- * ei_sparse_prefill_attn.
+ * compute only its own blocks.  Same arguments (without a workspace: a static
+ * grid) and bitwise the same output as ei_sparse_prefill_attn.
  *
  * Errors: as ei_sparse_prefill_attn; EI_ERR_UNSUPPORTED also when
  * kmax > 128 or C_B > 8192 (the merged list lives in LDS).
@@ -294,8 +313,8 @@ ei_status ei_dense_prefill_attn(const uint16_t* q, const uint16_t* k, const uint
                                 ei_dims dims, float softmax_scale, int32_t causal,
                                 uint16_t* o, void* stream);
 
-/* Workspace bytes ei_entropy_guided_prefill needs (= ei_probe_workspace_bytes);
- * 0 on invalid sizes. */
+/* Workspace bytes ei_entropy_guided_prefill needs: ei_probe_workspace_bytes
+ * followed by EI_ATTN_WORKSPACE_BYTES for the attention; 0 on invalid sizes. */
 size_t ei_prefill_workspace_bytes(ei_dims dims, ei_tiling tiling);
 
 /*
@@ -309,7 +328,8 @@ size_t ei_prefill_workspace_bytes(ei_dims dims, ei_tiling tiling);
  *   params, mode, kmax as ei_select_blocks_mode
  *   log_scores, entropy, head_is_rigid, budget_blocks, block_idx, block_cnt,
  *   o                  outputs of the three calls (same layouts)
- *   workspace          at least ei_prefill_workspace_bytes()
+ *   workspace          at least ei_prefill_workspace_bytes(): the probe's
+ *                      workspace, then the attention's (persistent schedule)
  *
  * Errors: those of the three calls.
  */

@@ -84,7 +84,8 @@ def lib() -> ctypes.CDLL:
                                             _VP, _VP, ctypes.c_size_t, _VP]
         L.ei_sparse_prefill_attn.restype = ctypes.c_int
         L.ei_sparse_prefill_attn.argtypes = [_VP, _VP, _VP, Dims, Tiling, ctypes.c_float, _VP,
-                                             _VP, ctypes.c_int32, _VP, _VP]
+                                             _VP, ctypes.c_int32, _VP, _VP, ctypes.c_size_t,
+                                             _VP]
         L.ei_prefill_workspace_bytes.restype = ctypes.c_size_t
         L.ei_prefill_workspace_bytes.argtypes = [Dims, Tiling]
         L.ei_entropy_guided_prefill.restype = ctypes.c_int
@@ -97,7 +98,9 @@ def lib() -> ctypes.CDLL:
             _VP, _VP, _VP, Dims, Tiling, ctypes.c_double, BudgetParams, ctypes.c_int32,
             ctypes.c_int32, ctypes.c_float, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP]
         L.ei_sparse_prefill_attn_gqa_union.restype = ctypes.c_int
-        L.ei_sparse_prefill_attn_gqa_union.argtypes = L.ei_sparse_prefill_attn.argtypes
+        L.ei_sparse_prefill_attn_gqa_union.argtypes = [_VP, _VP, _VP, Dims, Tiling,
+                                                       ctypes.c_float, _VP, _VP, ctypes.c_int32,
+                                                       _VP, _VP]
         L.ei_dense_prefill_attn.restype = ctypes.c_int
         L.ei_dense_prefill_attn.argtypes = [_VP, _VP, _VP, Dims, ctypes.c_float, ctypes.c_int32,
                                             _VP, _VP]
@@ -305,10 +308,16 @@ def probe_select_fused(q, k, seg_len: int, block_len: int, e_t: float = 1e-5,
     return bufs["entropy"], {n: bufs[n] for n in ("rigid", "budget", "idx", "cnt")}
 
 
+ATTN_WORKSPACE_BYTES = 256   # EI_ATTN_WORKSPACE_BYTES
+
+
 def sparse_prefill_attn(q, k, v, block_idx, block_cnt, seg_len: int, block_len: int,
-                        softmax_scale: float | None = None, out=None, gqa_union: bool = False):
+                        softmax_scale: float | None = None, out=None, gqa_union: bool = False,
+                        persistent: bool = True, workspace=None):
     """ei_sparse_prefill_attn (or, with gqa_union, ei_sparse_prefill_attn_gqa_union,
-    bitwise the same result): bf16 [B,Hq,N,D] output."""
+    bitwise the same result): bf16 [B,Hq,N,D] output.  `persistent` passes a
+    scheduling workspace (`workspace`, or a new ATTN_WORKSPACE_BYTES one), which
+    selects the persistent grid; False passes none (the static grid)."""
     for t, n in ((q, "q"), (k, "k"), (v, "v")):
         _req(t, n, torch.bfloat16, 4)
     _req(block_idx, "block_idx", torch.int32, 4)
@@ -326,11 +335,22 @@ def sparse_prefill_attn(q, k, v, block_idx, block_cnt, seg_len: int, block_len: 
         raise ValueError("block_idx / block_cnt do not match [B, Hq, C_S]")
     sc = 1.0 / math.sqrt(d.head_dim) if softmax_scale is None else float(softmax_scale)
     _same_device(q, k, v, block_idx, block_cnt, out)
+    if persistent and not gqa_union and workspace is None:
+        workspace = torch.empty((ATTN_WORKSPACE_BYTES,), dtype=torch.uint8, device=q.device)
+    if workspace is not None:
+        _same_device(q, workspace)
     with torch.cuda.device(q.device):
-        fn = "ei_sparse_prefill_attn_gqa_union" if gqa_union else "ei_sparse_prefill_attn"
-        st = getattr(lib(), fn)(_ptr(q), _ptr(k), _ptr(v), d, Tiling(seg_len, block_len), sc,
-                                _ptr(block_idx), _ptr(block_cnt), int(block_idx.shape[-1]),
-                                _ptr(out), _stream(q))
+        args = [_ptr(q), _ptr(k), _ptr(v), d, Tiling(seg_len, block_len), sc, _ptr(block_idx),
+                _ptr(block_cnt), int(block_idx.shape[-1]), _ptr(out)]
+        if gqa_union:
+            fn = "ei_sparse_prefill_attn_gqa_union"
+            st = lib().ei_sparse_prefill_attn_gqa_union(*args, _stream(q))
+        else:
+            fn = "ei_sparse_prefill_attn"
+            ws = workspace if persistent else None
+            nb = ws.numel() * ws.element_size() if ws is not None else 0
+            st = lib().ei_sparse_prefill_attn(*args, _ptr(ws) if ws is not None else None, nb,
+                                              _stream(q))
     _check(fn, st)
     return out
 

@@ -10,7 +10,8 @@
 
 namespace {
 
-constexpr int32_t kAbiVersion = 6;
+constexpr int32_t kAbiVersion = 7;
+static_assert(EI_ATTN_WORKSPACE_BYTES == ei::kAttnSchedBytes, "attention workspace size");
 
 struct Sizes {
   int64_t B, Hq, Hkv, N, D, CS, CB, r;
@@ -222,7 +223,8 @@ ei_status ei_probe_select_fused(const uint16_t* q, const uint16_t* k, ei_dims di
 ei_status ei_sparse_prefill_attn(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                                  ei_dims dims, ei_tiling tiling, float softmax_scale,
                                  const int32_t* block_idx, const int32_t* block_cnt,
-                                 int32_t kmax, uint16_t* o, void* stream) {
+                                 int32_t kmax, uint16_t* o, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
   ei_status st = check_dims(dims);
   if (st != EI_OK) return st;
   if ((st = check_tiling(tiling)) != EI_OK) return st;
@@ -231,10 +233,12 @@ ei_status ei_sparse_prefill_attn(const uint16_t* q, const uint16_t* k, const uin
   if (z.B == 0 || z.N == 0) return EI_OK;
   if (!q || !k || !v || !block_idx || !block_cnt || !o) return EI_ERR_NULL;
   if (!aligned16({q, k, v, o}) || !aligned4({block_idx, block_cnt})) return EI_ERR_UNSUPPORTED;
+  if (workspace && workspace_bytes < EI_ATTN_WORKSPACE_BYTES) return EI_ERR_WORKSPACE;
+  if (workspace && !aligned16({workspace})) return EI_ERR_UNSUPPORTED;
   const ei::AttnShape as{(int)z.B, (int)z.Hq, (int)z.Hkv, (int)z.N, tiling.seg_len,
                          tiling.block_len, (int)z.CS, (int)z.CB, kmax, softmax_scale};
   return from_hip(ei::launch_attention(q, k, v, as, ei::kSparse, block_idx, block_cnt, o,
-                                       (hipStream_t)stream));
+                                       workspace, (hipStream_t)stream));
 }
 
 ei_status ei_sparse_prefill_attn_gqa_union(const uint16_t* q, const uint16_t* k,
@@ -258,7 +262,10 @@ ei_status ei_sparse_prefill_attn_gqa_union(const uint16_t* q, const uint16_t* k,
 }
 
 size_t ei_prefill_workspace_bytes(ei_dims dims, ei_tiling tiling) {
-  return ei_probe_workspace_bytes(dims, tiling);
+  // the probe workspace (a multiple of 256 bytes), then the attention's
+  // scheduling counters
+  const size_t p = ei_probe_workspace_bytes(dims, tiling);
+  return p ? p + EI_ATTN_WORKSPACE_BYTES : 0;
 }
 
 ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const uint16_t* v,
@@ -292,7 +299,9 @@ ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const 
                            params.alpha, params.delta_t, params.base_budget_tokens,
                            params.max_budget_mult, (int)mode, (int)(z.Hq / z.Hkv)};
   if (!ei::select_supported(ss)) return EI_ERR_UNSUPPORTED;
-  if (!workspace || workspace_bytes < ei::probe_workspace_bytes(ps)) return EI_ERR_WORKSPACE;
+  const size_t probe_bytes = ei::probe_workspace_bytes(ps);
+  if (!workspace || workspace_bytes < probe_bytes + EI_ATTN_WORKSPACE_BYTES)
+    return EI_ERR_WORKSPACE;
   if (!aligned16({workspace})) return EI_ERR_UNSUPPORTED;
   const ei::AttnShape as{(int)z.B, (int)z.Hq, (int)z.Hkv, (int)z.N, tiling.seg_len,
                          tiling.block_len, (int)z.CS, (int)z.CB, kmax, softmax_scale};
@@ -306,7 +315,8 @@ ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const 
     err = ei::launch_select(log_scores, entropy, ss, head_is_rigid, budget_blocks, block_idx,
                             block_cnt, s0);
   if (err == hipSuccess)
-    err = ei::launch_attention(q, k, v, as, ei::kSparse, block_idx, block_cnt, o, s0);
+    err = ei::launch_attention(q, k, v, as, ei::kSparse, block_idx, block_cnt, o,
+                               (unsigned char*)workspace + probe_bytes, s0);
   return from_hip(err);
 }
 
@@ -324,7 +334,7 @@ ei_status ei_dense_prefill_attn(const uint16_t* q, const uint16_t* k, const uint
                          softmax_scale};
   return from_hip(ei::launch_attention(q, k, v, as,
                                        causal ? ei::kDenseCausal : ei::kDenseFull, nullptr,
-                                       nullptr, o, (hipStream_t)stream));
+                                       nullptr, o, nullptr, (hipStream_t)stream));
 }
 
 }  // extern "C"

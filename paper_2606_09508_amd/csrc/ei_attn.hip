@@ -26,11 +26,18 @@
 // Dense workgroups are mapped so that each XCD (dispatched round-robin)
 // receives a contiguous run of (batch, KV head, tile, query head) work: the G
 // query heads that share a K/V head, and neighbouring tiles, run on one XCD
-// and reuse K/V blocks from its L2.  Sparse work per head is uneven (budgets
-// differ per head, up to 3x), so a fixed head -> XCD assignment leaves the
-// XCD with the heaviest heads finishing last; instead the KV groups rotate
-// over the XCDs every 4 tiles.  Heavier (later) tiles are issued
-// first in both.
+// and reuse K/V blocks from its L2.  Heavier (later) tiles are issued first.
+//
+// Sparse work per head is uneven (budgets differ per head, up to 3x).  With a
+// scheduling workspace the sparse kernel is persistent: two workgroups per
+// CU, each taking (tile, KV group, query head) items from a queue of its own
+// XCD (the XCD's KV groups, or its share of one group's tiles in runs of
+// kRun, heaviest tile first) through an atomic counter, and from the other
+// XCDs' queues once its own is empty.  Each XCD's L2 then holds the K/V of
+// its own groups, whose tiles select largely the same blocks, and the
+// stealing evens out the groups' different loads.  Without a workspace (or
+// for KV-group counts that do not tile the XCDs) the grid is static: the KV
+// groups rotate over the XCDs every 4 tiles, heaviest tiles first.
 #include "ei_internal.h"
 
 #include <math.h>
@@ -47,7 +54,8 @@ constexpr int kThreads = 256;
 constexpr int kTileQ = 128;
 constexpr int kSub = 64;            // keys per staged sub-block
 constexpr int kXcds = 8;
-constexpr unsigned kRotRun = 4;    // tiles a KV group stays on one XCD (sparse)
+constexpr unsigned kRotRun = 4;    // tiles a KV group stays on one XCD (static sparse grid)
+constexpr unsigned kRun = 16;      // tile run per XCD when XCDs share a KV group (persistent)
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 w) { return __builtin_bit_cast(bf16x8, w); }
 
@@ -175,6 +183,41 @@ __device__ __forceinline__ bf16x8 read_vt(const unsigned char* stage, int dt, in
 // (gfx9 encoding: vmcnt in bits 3:0 and 15:14; expcnt, lgkmcnt left at max).
 #define EI_WAIT_VMCNT(n) \
   __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (7 << 4) | (15 << 8))
+
+// The persistent sparse schedule (see the file comment).  S = 1: XCD x owns
+// the KV groups x, x + 8, ... (ngx of them); S > 1 (8 = S x the number of
+// groups): XCD x owns group x % NG and, of its tiles ranked heaviest first,
+// the runs of kRun ranks with (rank / kRun) % S == x / NG.  per_x[x] is the
+// length of XCD x's queue.  Every item appears in exactly one queue.
+struct XcdPlan {
+  unsigned S, ngx, per_x[kXcds];
+};
+
+// Item idx of XCD x's queue -> (tile, query head in the group, KV group).
+__device__ __forceinline__ void plan_item(const XcdPlan& pl, unsigned x, unsigned idx, int n_tiles,
+                                          unsigned G, unsigned NG, int& tile, int& hh,
+                                          unsigned& bg) {
+  unsigned tr;
+  if (pl.S == 1) {
+    const unsigned per_rank = G * pl.ngx;
+    tr = idx / per_rank;
+    const unsigned rem = idx % per_rank;
+    hh = (int)(rem % G);
+    bg = x + kXcds * (rem / G);
+  } else {
+    const unsigned kq = idx / G, part = x / NG;
+    hh = (int)(idx % G);
+    bg = x % NG;
+    tr = (kq / kRun) * (pl.S * kRun) + part * kRun + kq % kRun;
+  }
+  tile = n_tiles - 1 - (int)tr;
+}
+
+// Queue counters of one call (the caller's scheduling workspace), zeroed on
+// the call's stream before the kernel reads them.
+__global__ void sched_reset_kernel(uint32_t* __restrict__ sched) {
+  if (threadIdx.x < kXcds) sched[threadIdx.x] = 0u;
+}
 
 // Lazy rescaling: the running maximum m is only raised when a new score
 // exceeds it by more than 8 (base-2 units), so O and l are rescaled rarely; O
@@ -317,16 +360,46 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ v, uint16_t* __restrict__ o, int B, int Hq, int Hkv, int N,
     int n_tiles, int Ls, int CS, int CB, float sc_log2, const int32_t* __restrict__ bidx,
-    const int32_t* __restrict__ bcnt, int kmax) {
+    const int32_t* __restrict__ bcnt, int kmax, uint32_t* __restrict__ sched,
+    const XcdPlan plan) {
   // two LDS objects (not one array) so that the compiler can tell the copy
   // into one stage from the reads of the other
   __shared__ __attribute__((aligned(1024))) unsigned char stage0[kStageBytes];
   __shared__ __attribute__((aligned(1024))) unsigned char stage1[kStageBytes];
+  __shared__ unsigned s_x, s_idx;   // the persistent workgroup's next item
 
   const unsigned G = (unsigned)(Hq / Hkv);
   const unsigned total = (unsigned)B * (unsigned)Hq * (unsigned)n_tiles;
+  const bool pers = MODE == kSparse && sched != nullptr;
+  // this workgroup's XCD (XCC_ID register): its own queue comes first
+  const unsigned x0 = pers ? (__builtin_amdgcn_s_getreg((31 << 11) | 20) & (kXcds - 1)) : 0u;
+  for (;;) {
   int hh, tile, g, b;
-  if (MODE != kSparse) {
+  if (pers) {
+    if (threadIdx.x == 0) {
+      unsigned xs = kXcds, is = 0;
+      for (unsigned d = 0; d < kXcds && xs == kXcds; ++d) {
+        const unsigned x = (x0 + d) & (kXcds - 1);
+        if (plan.per_x[x] == 0) continue;
+        const unsigned t = atomicAdd(&sched[x], 1u);
+        if (t < plan.per_x[x]) {
+          xs = x;
+          is = t;
+        }
+      }
+      s_x = xs;
+      s_idx = is;
+    }
+    // (the previous item's closing barrier keeps this write after every
+    // wave's read of the last item)
+    __syncthreads();
+    const unsigned xs = s_x;
+    if (xs == kXcds) return;   // every queue is empty
+    unsigned bg;
+    plan_item(plan, xs, s_idx, n_tiles, G, (unsigned)(B * Hkv), tile, hh, bg);
+    b = (int)(bg / (unsigned)Hkv);
+    g = (int)(bg % (unsigned)Hkv);
+  } else if (MODE != kSparse) {
     const unsigned per_xcd = gridDim.x / kXcds;
     unsigned t = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
     if (t >= total) return;
@@ -445,20 +518,63 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(
     if (i + 1 < n_steps) step(i + 1, stage1);
   }
 
-  if (qrow >= N) return;
-  store_rows(o, (size_t)(b * Hq + h) * N + qrow, hf, oacc, l_i);
+  if (qrow < N) store_rows(o, (size_t)(b * Hq + h) * N + qrow, hf, oacc, l_i);
+  if (!pers) return;
+  __syncthreads();   // every wave is done with the stages (and the item)
+  }
+}
+
+// The persistent plan for a shape, if its KV groups tile the XCDs.
+bool make_plan(const AttnShape& s, int n_tiles, XcdPlan& pl) {
+  const unsigned NG = (unsigned)(s.B * s.Hkv), G = (unsigned)(s.Hq / s.Hkv);
+  if (NG % kXcds == 0) {
+    pl.S = 1;
+    pl.ngx = NG / kXcds;
+    for (unsigned x = 0; x < kXcds; ++x) pl.per_x[x] = (unsigned)n_tiles * G * pl.ngx;
+    return true;
+  }
+  if (kXcds % NG != 0) return false;
+  pl.S = kXcds / NG;
+  pl.ngx = 1;
+  const unsigned cyc = pl.S * kRun, full = (unsigned)n_tiles / cyc, rem = (unsigned)n_tiles % cyc;
+  for (unsigned x = 0; x < kXcds; ++x) {
+    const unsigned part = x / NG;
+    const unsigned tail = rem > part * kRun ? min(rem - part * kRun, kRun) : 0u;
+    pl.per_x[x] = G * (full * kRun + tail);
+  }
+  return true;
+}
+
+// Workgroups of the persistent grid: two per CU of the current device.
+int persistent_grid() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0)
+    return 0;
+  return 2 * cus;
 }
 
 template <int MODE, int SUB>
 hipError_t launch_t(const uint16_t* q, const uint16_t* k, const uint16_t* v, const AttnShape& s,
-                    const int32_t* bidx, const int32_t* bcnt, uint16_t* o, hipStream_t stream) {
+                    const int32_t* bidx, const int32_t* bcnt, uint16_t* o, uint32_t* sched,
+                    hipStream_t stream) {
   const int n_tiles = (s.N + kTileQ - 1) / kTileQ;
   const int64_t total = (int64_t)s.B * s.Hq * n_tiles;
-  const int64_t grid = (total + kXcds - 1) / kXcds * kXcds;
+  int64_t grid = (total + kXcds - 1) / kXcds * kXcds;
+  XcdPlan plan{};
+  int pgrid = 0;
+  if (MODE == kSparse && sched != nullptr && make_plan(s, n_tiles, plan) &&
+      (pgrid = persistent_grid()) > 0) {
+    hipLaunchKernelGGL(sched_reset_kernel, dim3(1), dim3(kWave), 0, stream, sched);
+    grid = grid < pgrid ? grid : (int64_t)pgrid;
+  } else {
+    sched = nullptr;
+  }
   const float sc_log2 = (float)((double)s.softmax_scale * 1.4426950408889634);
   hipLaunchKernelGGL((attn_kernel<MODE, SUB>), dim3((unsigned)grid), dim3(kThreads), 0, stream,
                      q, k, v, o, s.B, s.Hq, s.Hkv, s.N, n_tiles, s.Ls, s.CS, s.CB, sc_log2, bidx,
-                     bcnt, s.kmax);
+                     bcnt, s.kmax, sched, plan);
   return hipGetLastError();
 }
 
@@ -676,17 +792,19 @@ hipError_t launch_attention_union(const uint16_t* q, const uint16_t* k, const ui
 
 hipError_t launch_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                             const AttnShape& s, AttnMode mode, const int32_t* block_idx,
-                            const int32_t* block_cnt, uint16_t* o, hipStream_t stream) {
+                            const int32_t* block_cnt, uint16_t* o, void* sched_ws,
+                            hipStream_t stream) {
   if (s.B * (int64_t)s.Hq * ((s.N + kTileQ - 1) / kTileQ) >= (int64_t)1 << 31)
     return hipErrorInvalidValue;
+  uint32_t* sched = (uint32_t*)sched_ws;
   switch (mode) {
     case kSparse:
       return s.Lb == 2 * kSub
-                 ? launch_t<kSparse, 2>(q, k, v, s, block_idx, block_cnt, o, stream)
-                 : launch_t<kSparse, 1>(q, k, v, s, block_idx, block_cnt, o, stream);
+                 ? launch_t<kSparse, 2>(q, k, v, s, block_idx, block_cnt, o, sched, stream)
+                 : launch_t<kSparse, 1>(q, k, v, s, block_idx, block_cnt, o, sched, stream);
     case kDenseCausal:
-      return launch_t<kDenseCausal, 1>(q, k, v, s, nullptr, nullptr, o, stream);
-    default: return launch_t<kDenseFull, 1>(q, k, v, s, nullptr, nullptr, o, stream);
+      return launch_t<kDenseCausal, 1>(q, k, v, s, nullptr, nullptr, o, nullptr, stream);
+    default: return launch_t<kDenseFull, 1>(q, k, v, s, nullptr, nullptr, o, nullptr, stream);
   }
 }
 

@@ -167,8 +167,12 @@ hipError_t launch_attention_union(const uint16_t* q, const uint16_t* k, const ui
                                   const AttnShape& s, const int32_t* block_idx,
                                   const int32_t* block_cnt, uint16_t* o, hipStream_t stream);
 
+// sched_ws: the sparse kernel's scheduling workspace (kAttnSchedBytes, 4-byte
+// aligned) for its persistent grid, or null for the static grid.
+constexpr size_t kAttnSchedBytes = 256;
 hipError_t launch_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                             const AttnShape& s, AttnMode mode, const int32_t* block_idx,
-                            const int32_t* block_cnt, uint16_t* o, hipStream_t stream);
+                            const int32_t* block_cnt, uint16_t* o, void* sched_ws,
+                            hipStream_t stream);
 
 }  // namespace ei

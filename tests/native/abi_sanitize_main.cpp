@@ -103,18 +103,21 @@ int main() {
     EXPECT(ei_probe_select_fused(F16, F16, dd, t, 1.0, p, 0, km, FF, FU, FI, FI, FI, FV, fws,
                                  nullptr) < 0);
   // attention
-  EXPECT(ei_sparse_prefill_attn(F16, F16, F16, d, t, NAN, FI, FI, km, F16, nullptr) ==
-         EI_ERR_SHAPE);
-  EXPECT(ei_sparse_prefill_attn(F16, F16, F16, d, t, 0.088f, nullptr, FI, km, F16, nullptr) ==
-         EI_ERR_NULL);
-  EXPECT(ei_sparse_prefill_attn(F16, F16, F16, d, t, 0.088f, FI, FI, 0, F16, nullptr) < 0);
+  EXPECT(ei_sparse_prefill_attn(F16, F16, F16, d, t, NAN, FI, FI, km, F16, nullptr, 0,
+                                nullptr) == EI_ERR_SHAPE);
+  EXPECT(ei_sparse_prefill_attn(F16, F16, F16, d, t, 0.088f, nullptr, FI, km, F16, nullptr, 0,
+                                nullptr) == EI_ERR_NULL);
+  EXPECT(ei_sparse_prefill_attn(F16, F16, F16, d, t, 0.088f, FI, FI, 0, F16, nullptr, 0,
+                                nullptr) < 0);
+  EXPECT(ei_sparse_prefill_attn(F16, F16, F16, d, t, 0.088f, FI, FI, km, F16, FV,
+                                EI_ATTN_WORKSPACE_BYTES - 1, nullptr) == EI_ERR_WORKSPACE);
   EXPECT(ei_dense_prefill_attn(F16, nullptr, F16, d, 0.088f, 1, F16, nullptr) == EI_ERR_NULL);
   EXPECT(ei_dense_prefill_attn(F16, F16, F16, d, NAN, 1, F16, nullptr) == EI_ERR_SHAPE);
   for (const ei_dims& dd : huge)
     EXPECT(ei_dense_prefill_attn(F16, F16, F16, dd, 0.088f, 1, F16, nullptr) < 0);
   // the one-call path
   const size_t pws = ei_prefill_workspace_bytes(d, t);
-  EXPECT(pws == ws);
+  EXPECT(pws == ws + EI_ATTN_WORKSPACE_BYTES);
   EXPECT(ei_entropy_guided_prefill(F16, F16, F16, d, t, 1.0, p, 0, km, 0.088f, FF, FF, FU, FI,
                                    FI, FI, F16, FV, pws - 1, nullptr) == EI_ERR_WORKSPACE);
   EXPECT(ei_entropy_guided_prefill(F16, F16, F16, d, t, 1.0, p, 7, km, 0.088f, FF, FF, FU, FI,
@@ -127,8 +130,8 @@ int main() {
 
   // scales: softmax_scale finite and > 0, probe_scale finite
   for (float sc : {0.0f, -0.088f, INFINITY, -INFINITY, NAN}) {
-    EXPECT(ei_sparse_prefill_attn(F16, F16, F16, d, t, sc, FI, FI, km, F16, nullptr) ==
-           EI_ERR_SHAPE);
+    EXPECT(ei_sparse_prefill_attn(F16, F16, F16, d, t, sc, FI, FI, km, F16, nullptr, 0,
+                                  nullptr) == EI_ERR_SHAPE);
     EXPECT(ei_dense_prefill_attn(F16, F16, F16, d, sc, 0, F16, nullptr) == EI_ERR_SHAPE);
     EXPECT(ei_entropy_guided_prefill(F16, F16, F16, d, t, 1.0, p, 0, km, sc, FF, FF, FU, FI, FI,
                                      FI, F16, FV, pws, nullptr) == EI_ERR_SHAPE);

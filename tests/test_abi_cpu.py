@@ -35,7 +35,7 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_helpers(L):
-    assert L.ei_abi_version() == 6
+    assert L.ei_abi_version() == 7
     assert eb.kmax(128, 64, 2048, 3) == 98
     assert eb.kmax(2048, 64, 2048, 3) == 96 + 32
     assert eb.kmax(256, 128, 256, 3) == 6 + 2
@@ -88,7 +88,7 @@ def test_empty_problems_launch_nothing(L):
         assert L.ei_select_blocks(None, None, d, t, eb.budget_params(), 98, None, None, None,
                                   None, None) == 0
         assert L.ei_sparse_prefill_attn(None, None, None, d, t, 0.088, None, None, 98, None,
-                                        None) == 0
+                                        None, 0, None) == 0
         assert L.ei_dense_prefill_attn(None, None, None, d, 0.088, 1, None, None) == 0
 
 
@@ -112,11 +112,16 @@ def test_select_rejects_bad_params(L):
 
 def test_attention_rejects_bad_arguments(L):
     d, t = eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(128, 64)
-    assert L.ei_sparse_prefill_attn(FAKE, FAKE, FAKE, d, t, 0.088, FAKE, FAKE, 0, FAKE, None) == -2
-    assert L.ei_sparse_prefill_attn(FAKE, FAKE, FAKE, d, t, 0.088, None, FAKE, 10, FAKE,
-                                    None) == -1
-    assert L.ei_sparse_prefill_attn(FAKE, FAKE, FAKE, eb.Dims(1, 4, 1, 1024, 96), t, 0.088, FAKE,
-                                    FAKE, 10, FAKE, None) == -3
+    spa = L.ei_sparse_prefill_attn
+    assert spa(FAKE, FAKE, FAKE, d, t, 0.088, FAKE, FAKE, 0, FAKE, None, 0, None) == -2
+    assert spa(FAKE, FAKE, FAKE, d, t, 0.088, None, FAKE, 10, FAKE, None, 0, None) == -1
+    assert spa(FAKE, FAKE, FAKE, eb.Dims(1, 4, 1, 1024, 96), t, 0.088, FAKE, FAKE, 10, FAKE,
+               None, 0, None) == -3
+    # the scheduling workspace: EI_ATTN_WORKSPACE_BYTES, 16-byte aligned
+    assert spa(FAKE, FAKE, FAKE, d, t, 0.088, FAKE, FAKE, 10, FAKE, FAKE,
+               eb.ATTN_WORKSPACE_BYTES - 1, None) == -4
+    assert spa(FAKE, FAKE, FAKE, d, t, 0.088, FAKE, FAKE, 10, FAKE, _off(FAKE, 4),
+               eb.ATTN_WORKSPACE_BYTES, None) == -3
     assert L.ei_dense_prefill_attn(FAKE, FAKE, None, d, 0.088, 1, FAKE, None) == -1
     assert L.ei_dense_prefill_attn(FAKE, FAKE, FAKE, eb.Dims(1, 5, 2, 64, 128), 0.088, 1, FAKE,
                                    None) == -2
@@ -128,7 +133,7 @@ def test_prefill_rejects_bad_arguments(L):
     p = eb.budget_params(base_budget=256)
     km = L.ei_kmax(t, p)
     ws = L.ei_prefill_workspace_bytes(d, t)
-    assert ws > 0 and ws == L.ei_probe_workspace_bytes(d, t)
+    assert ws > 0 and ws == L.ei_probe_workspace_bytes(d, t) + eb.ATTN_WORKSPACE_BYTES
     outs = (FAKE,) * 7
     call = L.ei_entropy_guided_prefill
     args = (FAKE, FAKE, FAKE, d, t, 1.0, p)
@@ -141,11 +146,14 @@ def test_prefill_rejects_bad_arguments(L):
 
 def test_prefill_workspace_is_the_probe_workspace(L):
     """The one-call path runs the three stages over the whole layer, so its
-    workspace is the whole problem's probe workspace."""
+    workspace is the whole problem's probe workspace followed by the
+    attention's scheduling workspace."""
     t = eb.Tiling(128, 64)
     for n in (1024, 8192, 16384, 131072):
         d = eb.Dims(2, 32, 8, n, 128)
-        assert L.ei_prefill_workspace_bytes(d, t) == L.ei_probe_workspace_bytes(d, t) > 0
+        pw = L.ei_probe_workspace_bytes(d, t)
+        assert pw > 0 and pw % 256 == 0
+        assert L.ei_prefill_workspace_bytes(d, t) == pw + eb.ATTN_WORKSPACE_BYTES
 
 
 def test_bench_refuses_several_gpus():
@@ -206,9 +214,12 @@ def test_misaligned_pointers_are_refused(L):
     assert sel(FAKE, FAKE, d, t, p, km, FAKE, FAKE, _off(FAKE, 1), FAKE, None) == -3
     assert sel(FAKE, FAKE, d, t, p, km, _off(FAKE, 1), FAKE, FAKE, _off(FAKE, 3), None) == -3
     spa = L.ei_sparse_prefill_attn
-    assert spa(FAKE, FAKE, _off(FAKE, 8), d, t, 0.088, FAKE, FAKE, km, FAKE, None) == -3
-    assert spa(FAKE, FAKE, FAKE, d, t, 0.088, FAKE, FAKE, km, _off(FAKE, 4), None) == -3
-    assert spa(FAKE, FAKE, FAKE, d, t, 0.088, _off(FAKE, 2), FAKE, km, FAKE, None) == -3
+    assert spa(FAKE, FAKE, _off(FAKE, 8), d, t, 0.088, FAKE, FAKE, km, FAKE, None, 0,
+               None) == -3
+    assert spa(FAKE, FAKE, FAKE, d, t, 0.088, FAKE, FAKE, km, _off(FAKE, 4), None, 0,
+               None) == -3
+    assert spa(FAKE, FAKE, FAKE, d, t, 0.088, _off(FAKE, 2), FAKE, km, FAKE, None, 0,
+               None) == -3
     assert L.ei_dense_prefill_attn(FAKE, _off(FAKE, 2), FAKE, d, 0.088, 1, FAKE, None) == -3
     assert L.ei_dense_prefill_attn(FAKE, FAKE, FAKE, d, 0.088, 0, _off(FAKE, 8), None) == -3
     ws = L.ei_prefill_workspace_bytes(d, t)
@@ -233,7 +244,7 @@ def test_sizes_whose_grids_overflow_are_refused(L):
     assert L.ei_entropy_probe(FAKE, FAKE, big, t, 1.0, FAKE, FAKE, FAKE, 1 << 30, None) == -2
     assert L.ei_dense_prefill_attn(FAKE, FAKE, FAKE, big, 0.088, 1, FAKE, None) == -2
     assert L.ei_sparse_prefill_attn(FAKE, FAKE, FAKE, big, t, 0.088, FAKE, FAKE, 98, FAKE,
-                                    None) == -2
+                                    None, 0, None) == -2
     ok = eb.Dims(1, 1 << 17, 1 << 10, 1 << 20, 128)       # 2^17 x 2^13 = 2^30 workgroups
     assert L.ei_num_segments(ok, t) == (1 << 20) // 128
 
@@ -292,7 +303,7 @@ def test_attention_refuses_non_positive_or_non_finite_scales(L, scale):
     d, t = eb.Dims(1, 4, 1, 1024, 128), eb.Tiling(128, 64)
     km = 98
     assert L.ei_sparse_prefill_attn(FAKE, FAKE, FAKE, d, t, scale, FAKE, FAKE, km, FAKE,
-                                    None) == -2
+                                    None, 0, None) == -2
     assert L.ei_sparse_prefill_attn_gqa_union(FAKE, FAKE, FAKE, d, t, scale, FAKE, FAKE, km,
                                               FAKE, None) == -2
     for causal in (0, 1):

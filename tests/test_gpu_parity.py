@@ -323,6 +323,40 @@ def test_gqa_union_attention_equals_per_head(wl, seed, case):
     assert err.max() <= ATTN_ABS
 
 
+@pytest.mark.parametrize("wl,seed,case", [
+    ("c1", 3, dict()),                                    # one KV group: 8 XCDs share it
+    ("c1", 3, dict(N=1000)),                              # ragged tail
+    ("c1", 4, dict(B=2, Hq=8, Hkv=2, N=3072)),            # four groups, two XCDs each
+    ("c1", 4, dict(B=2, Hq=16, Hkv=4, N=1024)),           # eight groups, one XCD each
+    ("c1", 5, dict(B=4, Hq=8, Hkv=4, N=640)),             # sixteen groups, two per XCD
+    ("c1", 5, dict(B=3, Hq=4, Hkv=1, N=384)),             # three groups: the static grid
+    ("c1", 6, dict(Ls=256, Lb=128, N=1280, base_budget=512)),   # two sub-blocks per block
+    ("c1", 6, dict(N=65)),
+    ("c2", 2, dict(N=16384)),
+    ("c4", 1, dict(N=8192)),                              # four KV groups, G = 7
+], ids=lambda x: x if isinstance(x, str) else None)
+def test_persistent_schedule_equals_static(wl, seed, case):
+    """With a scheduling workspace the sparse kernel runs persistent
+    workgroups over per-XCD queues with stealing; the output is bitwise the
+    static grid's (no workspace), also on a second call into the same
+    workspace (the counters are reset by each call)."""
+    w = synth.make(wl, seed, **case)
+    say(f"[persistent] {wl} seed={seed} {case}")
+    q, k, v = to_dev(w.q), to_dev(w.k), to_dev(w.v)
+    ls, en = eb.entropy_probe(q, k, w.Ls, w.Lb, w.probe_scale)
+    sel = eb.select_blocks(ls, en, w.N, w.Ls, w.Lb, w.e_t, w.alpha, w.delta_t, w.base_budget,
+                           w.mult, n_kv_heads=w.Hkv)
+    o_static = eb.sparse_prefill_attn(q, k, v, sel["idx"], sel["cnt"], w.Ls, w.Lb,
+                                      w.softmax_scale, persistent=False)
+    ws = torch.empty((eb.ATTN_WORKSPACE_BYTES,), dtype=torch.uint8, device=q.device)
+    for call in range(2):
+        o = torch.full_like(q, float("nan"))
+        eb.sparse_prefill_attn(q, k, v, sel["idx"], sel["cnt"], w.Ls, w.Lb, w.softmax_scale,
+                               out=o, workspace=ws)
+        torch.cuda.synchronize()
+        assert torch.equal(o, o_static), f"call {call}"
+
+
 def test_binding_refuses_mismatched_tensors():
     """k / v / score tensors that do not match q's sizes raise before any launch."""
     w = synth.make("c1", 4, N=512)
@@ -600,6 +634,13 @@ def test_c3_llama8b_128k(c3):
     rows = _spread_query_rows(w, 4096, seed=3)
     amax, amean = check_attention(w, r, rows)
     say(f"  attn ({len(rows)} rows) max {amax:.2e} mean {amean:.2e}")
+    # the persistent schedule (the path's) against the static grid, whole layer
+    sel = {kk: torch.from_numpy(t).to(r["q"].device) for kk, t in r["sel"].items()}
+    o_static = eb.sparse_prefill_attn(r["q"], r["k"], r["v"], sel["idx"], sel["cnt"], w.Ls,
+                                      w.Lb, w.softmax_scale, persistent=False)
+    torch.cuda.synchronize()
+    assert torch.equal(o_static, r["o"])
+    say("  persistent schedule bitwise equal to the static grid")
 
 
 def _fused_equals_path(w, r):
