@@ -32,7 +32,7 @@
 // scheduling workspace the sparse kernel is persistent: two workgroups per
 // CU, each taking (tile, KV group, query head) items from a queue of its own
 // XCD (the XCD's KV groups, or its share of one group's tiles in runs of
-// kRun, heaviest tile first) through an atomic counter, and from the other
+// kRun, heaviest tiles first) through an atomic counter, and from the other
 // XCDs' queues once its own is empty.  Each XCD's L2 then holds the K/V of
 // its own groups, whose tiles select largely the same blocks, and the
 // stealing evens out the groups' different loads.  Without a workspace (or
@@ -56,6 +56,7 @@ constexpr int kSub = 64;            // keys per staged sub-block
 constexpr int kXcds = 8;
 constexpr unsigned kRotRun = 4;    // tiles a KV group stays on one XCD (static sparse grid)
 constexpr unsigned kRun = 16;      // tile run per XCD when XCDs share a KV group (persistent)
+constexpr unsigned kHeadRun = 16;  // tiles of one query head in a row in an XCD's queue
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 w) { return __builtin_bit_cast(bf16x8, w); }
 
@@ -185,10 +186,15 @@ __device__ __forceinline__ bf16x8 read_vt(const unsigned char* stage, int dt, in
   __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (7 << 4) | (15 << 8))
 
 // The persistent sparse schedule (see the file comment).  S = 1: XCD x owns
-// the KV groups x, x + 8, ... (ngx of them); S > 1 (8 = S x the number of
-// groups): XCD x owns group x % NG and, of its tiles ranked heaviest first,
-// the runs of kRun ranks with (rank / kRun) % S == x / NG.  per_x[x] is the
-// length of XCD x's queue.  Every item appears in exactly one queue.
+// the KV groups x, x + 8, ... (ngx of them), its queue running over chunks of
+// kHeadRun tile ranks (heaviest first) and, inside a chunk, over its (group,
+// query head) pairs, each taking the chunk's tiles in a row (at the 128k
+// layer: 10.5 GB fetched per launch against 13.7 GB with the heads of a
+// tile next to each other, and equal or 1-2% faster).  S > 1 (8 = S x the
+// number of groups): XCD x owns group x % NG and, of its tiles ranked
+// heaviest first, the runs of kRun ranks with (rank / kRun) % S == x / NG.
+// per_x[x] is the length of XCD x's queue.  Every item appears in exactly
+// one queue.
 struct XcdPlan {
   unsigned S, ngx, per_x[kXcds];
 };
@@ -199,11 +205,15 @@ __device__ __forceinline__ void plan_item(const XcdPlan& pl, unsigned x, unsigne
                                           unsigned& bg) {
   unsigned tr;
   if (pl.S == 1) {
+    // chunks of kHeadRun tile ranks, heaviest first; inside a chunk the
+    // (group, head) pairs in turn, each over the chunk's ranks
     const unsigned per_rank = G * pl.ngx;
-    tr = idx / per_rank;
-    const unsigned rem = idx % per_rank;
-    hh = (int)(rem % G);
-    bg = x + kXcds * (rem / G);
+    const unsigned c = idx / (kHeadRun * per_rank), j = idx % (kHeadRun * per_rank);
+    const unsigned rr = min(kHeadRun, (unsigned)n_tiles - c * kHeadRun);   // ranks in the chunk
+    const unsigned hg = j / rr;
+    tr = c * kHeadRun + j % rr;
+    hh = (int)(hg % G);
+    bg = x + kXcds * (hg / G);
   } else {
     const unsigned kq = idx / G, part = x / NG;
     hh = (int)(idx % G);
