@@ -342,15 +342,15 @@ ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const 
                                     void* workspace, size_t workspace_bytes, void* stream);
 
 /* Device scratch that ei_entropy_guided_prefill_noalloc holds on every device
- * it runs on, until the process ends (128 MiB: the probe workspace of a layer
- * of 64 query and 8 KV heads at 131072 tokens is 123 MiB). */
+ * it runs on, until the process ends (128 MiB: the workspace of a layer of 64
+ * query and 8 KV heads at 131072 tokens is 123 MiB). */
 #define EI_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
 
 /*
  * ei_entropy_guided_prefill_noalloc -- ei_entropy_guided_prefill for callers
  * that cannot allocate device memory: work captured into a HIP graph, tight
  * serving loops, harnesses that forbid hipMalloc.  The same arguments and
- * bitwise the same outputs, without the workspace: the probe workspace is a
+ * bitwise the same outputs, without the workspace: the workspace (probe and attention) is a
  * static device array of EI_NOALLOC_SCRATCH_BYTES per device (looked up on the
  * first call on a device, with that device current).  The call allocates and
  * frees nothing.  Every call on a device shares that device's array, so calls
