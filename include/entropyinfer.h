@@ -350,9 +350,9 @@ ei_status ei_entropy_guided_prefill(const uint16_t* q, const uint16_t* k, const 
  * ei_entropy_guided_prefill_noalloc -- ei_entropy_guided_prefill for callers
  * that cannot allocate device memory: work captured into a HIP graph, tight
  * serving loops, harnesses that forbid hipMalloc.  The same arguments and
- * bitwise the same outputs, without the workspace: the workspace (probe and attention) is a
- * static device array of EI_NOALLOC_SCRATCH_BYTES per device (looked up on the
- * first call on a device, with that device current).  The call allocates and
+ * bitwise the same outputs, without the workspace: the workspace (the probe's
+ * and the attention's) is a static device array of EI_NOALLOC_SCRATCH_BYTES per
+ * device (looked up on the first call on a device, with that device current).  The call allocates and
  * frees nothing.  Every call on a device shares that device's array, so calls
  * that overlap on one device (on different streams, or from several threads)
  * race and must be serialised by the caller.
