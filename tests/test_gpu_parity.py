@@ -330,6 +330,8 @@ def test_gqa_union_attention_equals_per_head(wl, seed, case):
     ("c1", 4, dict(B=2, Hq=16, Hkv=4, N=1024)),           # eight groups, one XCD each
     ("c1", 5, dict(B=4, Hq=8, Hkv=4, N=640)),             # sixteen groups, two per XCD
     ("c1", 5, dict(B=3, Hq=4, Hkv=1, N=384)),             # three groups: the static grid
+    ("c1", 7, dict(B=2, Hq=4, Hkv=1, N=2560)),            # two groups, four XCDs each
+    ("c1", 7, dict(B=3, Hq=16, Hkv=8, N=256)),            # 24 groups, three per XCD
     ("c1", 6, dict(Ls=256, Lb=128, N=1280, base_budget=512)),   # two sub-blocks per block
     ("c1", 6, dict(N=65)),
     ("c2", 2, dict(N=16384)),
