@@ -182,6 +182,8 @@ def main():
                 "idx": torch.empty((w.B, w.Hq, w.CS, w.kmax), dtype=torch.int32, device=dev),
                 "cnt": torch.empty((w.B, w.Hq, w.CS), dtype=torch.int32, device=dev)},
         "out": torch.empty_like(q),
+        # the sparse attention's scheduling workspace (persistent grid)
+        "attn_ws": torch.empty((eb.ATTN_WORKSPACE_BYTES,), dtype=torch.uint8, device=dev),
     }
 
     def step(ev=None):
@@ -196,7 +198,7 @@ def main():
         if ev is not None:
             ev[2].record()
         eb.sparse_prefill_attn(q, k, v, bufs["sel"]["idx"], bufs["sel"]["cnt"], w.Ls, w.Lb,
-                               w.softmax_scale, bufs["out"])
+                               w.softmax_scale, bufs["out"], workspace=bufs["attn_ws"])
         if ev is not None:
             ev[3].record()
 
@@ -427,6 +429,7 @@ def time_path(w, q, k, v, Ls, Lb, base_budget, e_t, mode, steps, warmup):
            "idx": torch.empty((w.B, w.Hq, CS, km), dtype=torch.int32, device=dev),
            "cnt": torch.empty((w.B, w.Hq, CS), dtype=torch.int32, device=dev)}
     o = torch.empty_like(q)
+    attn_ws = torch.empty((eb.ATTN_WORKSPACE_BYTES,), dtype=torch.uint8, device=dev)
 
     def one(ev=None):
         if ev is not None:
@@ -438,7 +441,8 @@ def time_path(w, q, k, v, Ls, Lb, base_budget, e_t, mode, steps, warmup):
                          n_kv_heads=w.Hkv, out=sel, mode=mode)
         if ev is not None:
             ev[2].record()
-        eb.sparse_prefill_attn(q, k, v, sel["idx"], sel["cnt"], Ls, Lb, w.softmax_scale, o)
+        eb.sparse_prefill_attn(q, k, v, sel["idx"], sel["cnt"], Ls, Lb, w.softmax_scale, o,
+                               workspace=attn_ws)
         if ev is not None:
             ev[3].record()
 
