@@ -384,153 +384,153 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(
   // this workgroup's XCD (XCC_ID register): its own queue comes first
   const unsigned x0 = pers ? (__builtin_amdgcn_s_getreg((31 << 11) | 20) & (kXcds - 1)) : 0u;
   for (;;) {
-  int hh, tile, g, b;
-  if (pers) {
-    if (threadIdx.x == 0) {
-      unsigned xs = kXcds, is = 0;
-      for (unsigned d = 0; d < kXcds && xs == kXcds; ++d) {
-        const unsigned x = (x0 + d) & (kXcds - 1);
-        if (plan.per_x[x] == 0) continue;
-        const unsigned t = atomicAdd(&sched[x], 1u);
-        if (t < plan.per_x[x]) {
-          xs = x;
-          is = t;
+    int hh, tile, g, b;
+    if (pers) {
+      if (threadIdx.x == 0) {
+        unsigned xs = kXcds, is = 0;
+        for (unsigned d = 0; d < kXcds && xs == kXcds; ++d) {
+          const unsigned x = (x0 + d) & (kXcds - 1);
+          if (plan.per_x[x] == 0) continue;
+          const unsigned t = atomicAdd(&sched[x], 1u);
+          if (t < plan.per_x[x]) {
+            xs = x;
+            is = t;
+          }
         }
+        s_x = xs;
+        s_idx = is;
       }
-      s_x = xs;
-      s_idx = is;
+      // (the previous item's closing barrier keeps this write after every
+      // wave's read of the last item)
+      __syncthreads();
+      const unsigned xs = s_x;
+      if (xs == kXcds) return;   // every queue is empty
+      unsigned bg;
+      plan_item(plan, xs, s_idx, n_tiles, G, (unsigned)(B * Hkv), tile, hh, bg);
+      b = (int)(bg / (unsigned)Hkv);
+      g = (int)(bg % (unsigned)Hkv);
+    } else if (MODE != kSparse) {
+      const unsigned per_xcd = gridDim.x / kXcds;
+      unsigned t = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+      if (t >= total) return;
+      hh = (int)(t % G);
+      t /= G;
+      tile = n_tiles - 1 - (int)(t % (unsigned)n_tiles);
+      t /= (unsigned)n_tiles;
+      g = (int)(t % (unsigned)Hkv);
+      b = (int)(t / (unsigned)Hkv);
+    } else if (((unsigned)B * (unsigned)Hkv) % kXcds == 0) {
+      // Tile-major, heavier tiles first; for tile rank t, XCD x takes the KV
+      // groups bg with (bg + t / kRotRun) % 8 == x (all G query heads of each):
+      // a group stays on one XCD for kRotRun consecutive tiles (which select
+      // mostly the same blocks, so they share its L2) and then moves on, so
+      // every group's work is spread over all XCDs.
+      if (blockIdx.x >= total) return;
+      const unsigned x = blockIdx.x % kXcds, idx = blockIdx.x / kXcds;
+      const unsigned per_tile = ((unsigned)B * (unsigned)Hq) / kXcds;
+      const unsigned tr = idx / per_tile, rem = idx % per_tile;
+      tile = n_tiles - 1 - (int)tr;
+      hh = (int)(rem % G);
+      const unsigned rot = (tr / kRotRun) % kXcds;
+      const unsigned bg = (x + kXcds - rot) % kXcds + kXcds * (rem / G);
+      b = (int)(bg / (unsigned)Hkv);
+      g = (int)(bg % (unsigned)Hkv);
+    } else {
+      // Tile-major with the (batch, head) index rotated by one per tile.
+      if (blockIdx.x >= total) return;
+      const unsigned R = (unsigned)B * (unsigned)Hq;
+      const unsigned tr = blockIdx.x / R;
+      const unsigned r = (blockIdx.x % R + tr) % R;
+      tile = n_tiles - 1 - (int)tr;
+      b = (int)(r / (unsigned)Hq);
+      hh = (int)(r % (unsigned)Hq) % (int)G;
+      g = (int)(r % (unsigned)Hq) / (int)G;
     }
-    // (the previous item's closing barrier keeps this write after every
-    // wave's read of the last item)
-    __syncthreads();
-    const unsigned xs = s_x;
-    if (xs == kXcds) return;   // every queue is empty
-    unsigned bg;
-    plan_item(plan, xs, s_idx, n_tiles, G, (unsigned)(B * Hkv), tile, hh, bg);
-    b = (int)(bg / (unsigned)Hkv);
-    g = (int)(bg % (unsigned)Hkv);
-  } else if (MODE != kSparse) {
-    const unsigned per_xcd = gridDim.x / kXcds;
-    unsigned t = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
-    if (t >= total) return;
-    hh = (int)(t % G);
-    t /= G;
-    tile = n_tiles - 1 - (int)(t % (unsigned)n_tiles);
-    t /= (unsigned)n_tiles;
-    g = (int)(t % (unsigned)Hkv);
-    b = (int)(t / (unsigned)Hkv);
-  } else if (((unsigned)B * (unsigned)Hkv) % kXcds == 0) {
-    // Tile-major, heavier tiles first; for tile rank t, XCD x takes the KV
-    // groups bg with (bg + t / kRotRun) % 8 == x (all G query heads of each):
-    // a group stays on one XCD for kRotRun consecutive tiles (which select
-    // mostly the same blocks, so they share its L2) and then moves on, so
-    // every group's work is spread over all XCDs.
-    if (blockIdx.x >= total) return;
-    const unsigned x = blockIdx.x % kXcds, idx = blockIdx.x / kXcds;
-    const unsigned per_tile = ((unsigned)B * (unsigned)Hq) / kXcds;
-    const unsigned tr = idx / per_tile, rem = idx % per_tile;
-    tile = n_tiles - 1 - (int)tr;
-    hh = (int)(rem % G);
-    const unsigned rot = (tr / kRotRun) % kXcds;
-    const unsigned bg = (x + kXcds - rot) % kXcds + kXcds * (rem / G);
-    b = (int)(bg / (unsigned)Hkv);
-    g = (int)(bg % (unsigned)Hkv);
-  } else {
-    // Tile-major with the (batch, head) index rotated by one per tile.
-    if (blockIdx.x >= total) return;
-    const unsigned R = (unsigned)B * (unsigned)Hq;
-    const unsigned tr = blockIdx.x / R;
-    const unsigned r = (blockIdx.x % R + tr) % R;
-    tile = n_tiles - 1 - (int)tr;
-    b = (int)(r / (unsigned)Hq);
-    hh = (int)(r % (unsigned)Hq) % (int)G;
-    g = (int)(r % (unsigned)Hq) / (int)G;
-  }
-  const int h = g * (int)G + hh;
+    const int h = g * (int)G + hh;
 
-  const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
-  const int jq = lane & 31, hf = lane >> 5;
-  const int q0 = tile * kTileQ;
-  const int q_last = min(q0 + kTileQ - 1, N - 1);
-  const int qw0 = q0 + wave * 32;          // first query row of this wave
-  const int qrow = qw0 + jq;               // this lane's query row
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6, lane = tid & 63;
+    const int jq = lane & 31, hf = lane >> 5;
+    const int q0 = tile * kTileQ;
+    const int q_last = min(q0 + kTileQ - 1, N - 1);
+    const int qw0 = q0 + wave * 32;          // first query row of this wave
+    const int qrow = qw0 + jq;               // this lane's query row
 
-  const uint16_t* kh = k + (size_t)(b * Hkv + g) * N * kHeadDim;
-  const uint16_t* vh = v + (size_t)(b * Hkv + g) * N * kHeadDim;
+    const uint16_t* kh = k + (size_t)(b * Hkv + g) * N * kHeadDim;
+    const uint16_t* vh = v + (size_t)(b * Hkv + g) * N * kHeadDim;
 
-  // Q^T fragments (B operand of S^T = K Q^T), kept in registers.
-  bf16x8 qf[8];
-  {
-    const uint16_t* qp = q + ((size_t)(b * Hq + h) * N + qrow) * kHeadDim + 8 * hf;
-#pragma unroll
-    for (int s = 0; s < 8; ++s)
-      qf[s] = as_bf16x8(qrow < N ? *(const uint4*)(qp + 16 * s) : make_uint4(0, 0, 0, 0));
-  }
-
-  // The sub-blocks to visit.
-  const int32_t* lst = nullptr;
-  int n_steps;
-  if (MODE == kSparse) {
-    const int seg = q0 / Ls;
-    lst = bidx + ((size_t)(b * Hq + h) * CS + seg) * kmax;
-    const int c = min(max(bcnt[(size_t)(b * Hq + h) * CS + seg], 0), kmax);
-    n_steps = valid_prefix<SUB>(lst, c, CB, q_last, lane) * SUB;
-  } else if (MODE == kDenseCausal) {
-    n_steps = q_last / kSub + 1;
-  } else {
-    n_steps = (N + kSub - 1) / kSub;
-  }
-  auto step_key0 = [&](int i) -> int {
-    if (MODE == kSparse) return (SUB == 1 ? lst[i] : lst[i >> 1] * SUB + (i & 1)) * kSub;
-    return i * kSub;
-  };
-
-  // byte offsets of this lane's stage copies inside a 64-row block
-  uint32_t koff[4], voff[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int row = 16 * wave + 4 * j + (lane >> 4);
-    koff[j] = (uint32_t)(row * kRowBytes + 16 * swz(row, lane & 15));
-    voff[j] = (uint32_t)(row * kRowBytes + 16 * swz_v(row, lane & 15));
-  }
-
-  f32x16 oacc[4];
-#pragma unroll
-  for (int d = 0; d < 4; ++d)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) oacc[d][r] = 0.0f;
-  float m_i = -INFINITY, l_i = 0.0f;
-
-  // Two-stage LDS ring filled directly from global memory.  Step i waits for
-  // its stage (the 8 loads of step i+1 may still be in flight), computes, and
-  // after a second barrier refills the stage with step i+2.  Even steps use
-  // stage0, odd steps stage1.
-  auto step = [&](const int i, unsigned char* st) {
-    if (i + 1 < n_steps) EI_WAIT_VMCNT(8); else EI_WAIT_VMCNT(0);
-    __syncthreads();
-    const int k0 = step_key0(i);
-    const bool active = (MODE == kDenseFull) || (k0 <= qw0 + 31);
-    if (active && qw0 < N)
-      compute_step<MODE>(st, k0, qw0, qrow, N, jq, hf, lane, qf, sc_log2, oacc, m_i, l_i);
-    if (i + 2 < n_steps) {
-      __syncthreads();   // every wave is done reading this stage
-      issue_stage(st, kh, vh, step_key0(i + 2), N, wave, lane, koff, voff);
+    // Q^T fragments (B operand of S^T = K Q^T), kept in registers.
+    bf16x8 qf[8];
+    {
+      const uint16_t* qp = q + ((size_t)(b * Hq + h) * N + qrow) * kHeadDim + 8 * hf;
+  #pragma unroll
+      for (int s = 0; s < 8; ++s)
+        qf[s] = as_bf16x8(qrow < N ? *(const uint4*)(qp + 16 * s) : make_uint4(0, 0, 0, 0));
     }
-  };
-  // Q fragments (and the list) have landed before any stage copy is issued,
-  // so no later wait on them covers the copies in flight.
-  EI_WAIT_VMCNT(0);
-  if (n_steps > 0) issue_stage(stage0, kh, vh, step_key0(0), N, wave, lane, koff, voff);
-  if (n_steps > 1) issue_stage(stage1, kh, vh, step_key0(1), N, wave, lane, koff, voff);
-  for (int i = 0; i < n_steps; i += 2) {
-    step(i, stage0);
-    if (i + 1 < n_steps) step(i + 1, stage1);
-  }
 
-  if (qrow < N) store_rows(o, (size_t)(b * Hq + h) * N + qrow, hf, oacc, l_i);
-  if (!pers) return;
-  __syncthreads();   // every wave is done with the stages (and the item)
+    // The sub-blocks to visit.
+    const int32_t* lst = nullptr;
+    int n_steps;
+    if (MODE == kSparse) {
+      const int seg = q0 / Ls;
+      lst = bidx + ((size_t)(b * Hq + h) * CS + seg) * kmax;
+      const int c = min(max(bcnt[(size_t)(b * Hq + h) * CS + seg], 0), kmax);
+      n_steps = valid_prefix<SUB>(lst, c, CB, q_last, lane) * SUB;
+    } else if (MODE == kDenseCausal) {
+      n_steps = q_last / kSub + 1;
+    } else {
+      n_steps = (N + kSub - 1) / kSub;
+    }
+    auto step_key0 = [&](int i) -> int {
+      if (MODE == kSparse) return (SUB == 1 ? lst[i] : lst[i >> 1] * SUB + (i & 1)) * kSub;
+      return i * kSub;
+    };
+
+    // byte offsets of this lane's stage copies inside a 64-row block
+    uint32_t koff[4], voff[4];
+  #pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int row = 16 * wave + 4 * j + (lane >> 4);
+      koff[j] = (uint32_t)(row * kRowBytes + 16 * swz(row, lane & 15));
+      voff[j] = (uint32_t)(row * kRowBytes + 16 * swz_v(row, lane & 15));
+    }
+
+    f32x16 oacc[4];
+  #pragma unroll
+    for (int d = 0; d < 4; ++d)
+  #pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[d][r] = 0.0f;
+    float m_i = -INFINITY, l_i = 0.0f;
+
+    // Two-stage LDS ring filled directly from global memory.  Step i waits for
+    // its stage (the 8 loads of step i+1 may still be in flight), computes, and
+    // after a second barrier refills the stage with step i+2.  Even steps use
+    // stage0, odd steps stage1.
+    auto step = [&](const int i, unsigned char* st) {
+      if (i + 1 < n_steps) EI_WAIT_VMCNT(8); else EI_WAIT_VMCNT(0);
+      __syncthreads();
+      const int k0 = step_key0(i);
+      const bool active = (MODE == kDenseFull) || (k0 <= qw0 + 31);
+      if (active && qw0 < N)
+        compute_step<MODE>(st, k0, qw0, qrow, N, jq, hf, lane, qf, sc_log2, oacc, m_i, l_i);
+      if (i + 2 < n_steps) {
+        __syncthreads();   // every wave is done reading this stage
+        issue_stage(st, kh, vh, step_key0(i + 2), N, wave, lane, koff, voff);
+      }
+    };
+    // Q fragments (and the list) have landed before any stage copy is issued,
+    // so no later wait on them covers the copies in flight.
+    EI_WAIT_VMCNT(0);
+    if (n_steps > 0) issue_stage(stage0, kh, vh, step_key0(0), N, wave, lane, koff, voff);
+    if (n_steps > 1) issue_stage(stage1, kh, vh, step_key0(1), N, wave, lane, koff, voff);
+    for (int i = 0; i < n_steps; i += 2) {
+      step(i, stage0);
+      if (i + 1 < n_steps) step(i + 1, stage1);
+    }
+
+    if (qrow < N) store_rows(o, (size_t)(b * Hq + h) * N + qrow, hf, oacc, l_i);
+    if (!pers) return;
+    __syncthreads();   // every wave is done with the stages (and the item)
   }
 }
 
