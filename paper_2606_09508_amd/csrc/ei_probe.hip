@@ -867,7 +867,8 @@ __global__ __launch_bounds__(kThreads, MODE == kScoresSelect ? 1 : 4) void score
       if (u >= U) break;
       const int64_t row = unit_row(u);
       const float* rl = rows_lds + ul * row_cap;
-      topk::select_row<SLOTS>([&](int jj) { return rl[jj]; }, u / G, r, CB, kmax, kblocks[row],
+      topk::select_row<SLOTS>([&](int jj) { return rl[jj]; }, row_cap, u / G, r, CB, kmax,
+                              kblocks[row],
                               idx + row * (int64_t)kmax, cnt + row, hist, cand, lane);
     }
   }

@@ -3,9 +3,15 @@
 //
 //  budget_kernel  one workgroup per (b, query head): the rigid test over all
 //                 segment entropies, the ratios |e_s - e_{s-1}| / e_{s-1} in
-//                 parallel, the clamped budget recurrence (inherently
-//                 sequential; one wave, increments broadcast from LDS) and
-//                 k_s = min(floor(B_s / L_B), s r).
+//                 parallel, the clamped budget recurrence and
+//                 k_s = min(floor(B_s / L_B), s r).  The recurrence runs in
+//                 one wave, each lane owning a run of consecutive steps:
+//                 since one step x -> min(max(x + d, B_h), 3 B_h) is
+//                 monotone, a run evaluated from both ends of the clamp range
+//                 gives the true value wherever the two evaluations meet, so
+//                 a lane whose predecessor's run met knows its start at once;
+//                 the others wait for their predecessor, which is the
+//                 sequential order in the worst case.
 //                 Variants: the entropies may be the GQA group's means
 //                 (binary64 sum in head order / G, rounded to binary32), and
 //                 the rigid rule may apply per segment (B_s = B_h wherever
@@ -30,6 +36,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kChunk = 1024;
+constexpr int kRunMax = kChunk / kWave;   // steps per lane in the budget recurrence
 
 __global__ __launch_bounds__(kThreads) void budget_kernel(
     const float* __restrict__ entropy, int Hq, int CS, int r, int Lb, float e_t, double alpha,
@@ -37,6 +44,7 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(
     int32_t* __restrict__ k_out) {
   __shared__ double delta[kChunk];   // -inf: the segment restarts at B_h
   __shared__ double Bs[kChunk];
+  __shared__ float ent[kChunk];      // E(c0 + i) of the chunk at c0
   const int64_t bh = blockIdx.x;
   int32_t* ko = k_out + bh * CS;
   const int tid = threadIdx.x;
@@ -50,9 +58,14 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(
     return (float)(sum / (double)G);
   };
 
+  // the rigid test over every segment, keeping the first chunk's entropies
   int below = 1;
-  for (int s = tid; s < CS; s += kThreads)
-    if (!(E(s) < e_t)) below = 0;
+#pragma unroll 4
+  for (int s = tid; s < CS; s += kThreads) {
+    const float v = E(s);
+    if (s < kChunk) ent[s] = v;
+    if (!(v < e_t)) below = 0;
+  }
   below = __syncthreads_and(below);
   const double B0 = (double)Bh;
   const double cap = (double)mult * B0;
@@ -64,52 +77,95 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(
       ko[s] = (int32_t)min(kb, (int64_t)s * r);
     return;
   }
-  double Bprev = B0;   // meaningful in wave 0 only
+  double Bprev = B0;   // wave 0: B before the chunk's first step
   for (int c0 = 0; c0 < CS; c0 += kChunk) {
     const int n = min(kChunk, CS - c0);
-    // the increments are padded with zeros to a whole number of waves
+    // The steps are padded with zero increments to a whole number of waves
+    // (a zero increment leaves a clamped value unchanged) and split into
+    // kWave runs of L consecutive steps; step i = l L + j of lane l's run is
+    // held at delta[j kWave + l], so every lane's reads and writes of a step
+    // are one conflict-free row.
     const int npad = (n + kWave - 1) / kWave * kWave;
-    for (int i = tid; i < npad; i += kThreads) {
+    const int L = npad / kWave;
+    if (c0 > 0) {
+      for (int i = tid; i < n; i += kThreads) ent[i] = E(c0 + i);
+      __syncthreads();
+    }
+    for (int p = tid; p < npad; p += kThreads) {
+      const int i = (p % kWave) * L + p / kWave;
       if (i >= n) {
-        delta[i] = 0.0;
+        delta[p] = 0.0;
         continue;
       }
       const int s = c0 + i;
-      const float es = E(s);
+      const float es = ent[i];
       // B_0 = B_h, and a rigid segment of the per-segment rule takes B_h:
       // B_prev + (-inf) is clamped to exactly B_h below
       if (s == 0 || (mode == EI_CLASSIFY_SEGMENT && es < e_t)) {
-        delta[i] = -INFINITY;
+        delta[p] = -INFINITY;
         continue;
       }
-      const double ep = (double)E(s - 1), ec = (double)es;
+      const double ep = (double)(i > 0 ? ent[i - 1] : E(s - 1)), ec = (double)es;
       const double num = fabs(ec - ep);
       const double ratio = (num == 0.0 && ep == 0.0) ? 0.0 : num / ep;
       const double t = ratio - delta_t;
-      delta[i] = a * t;
+      delta[p] = a * t;
     }
     __syncthreads();
     if (tid < kWave) {
-      // Wave 0 runs the recurrence 64 segments at a time, every lane reading
-      // each increment from LDS as a broadcast (the loads of a group are
-      // independent of the chain and issue ahead of it), so the dependent
-      // chain is the add and the two clamps.  The clamps as fmax / fmin give
-      // the same value as the comparisons in every case (NaN and -inf -> B_0,
-      // +inf -> 3 B_0).  Every lane carries the same B_prev and writes the
-      // same value; past the chunk's end the steps run on the zero padding
-      // and their results are not read.
-      for (int i0 = 0; i0 < n; i0 += kWave) {
+      // One step of the recurrence.  The clamps as fmax / fmin give the same
+      // value as the comparisons in every case (NaN and -inf -> B_h, +inf ->
+      // 3 B_h), and every value a step yields lies in [lo, hi].
+      auto step = [&](double x, double d) { return fmin(fmax(x + d, B0), cap); };
+      const double lo = step(B0, -INFINITY), hi = step(B0, INFINITY);
+      const int lane = tid;
+      double dv[kRunMax];   // the lane's increments (entries j >= L unused)
 #pragma unroll
-        for (int j = 0; j < kWave; ++j) {
-          Bprev = fmin(fmax(Bprev + delta[i0 + j], B0), cap);
-          Bs[i0 + j] = Bprev;
+      for (int j = 0; j < kRunMax; ++j) dv[j] = delta[j * kWave + lane];
+      // A step is monotone in x, so a run evaluated from the two ends of an
+      // interval holding its true start bounds every true value of the run.
+      // Each round every lane runs its steps from both ends of its start
+      // interval, and its successor takes the two ends reached as its next
+      // start interval.  Lane 0 starts from the carried B itself; a lane whose
+      // start interval is one value (equal bit patterns) has its true start,
+      // and so does its successor one round later at the latest, so after at
+      // most kWave - 1 rounds every start is known.  Runs that meet a clamp
+      // from both ends settle their successors much sooner.  (The one thing
+      // the bounds cannot settle is the sign of a zero budget, which no k_s
+      // depends on.)
+      double pl = lane == 0 ? Bprev : lo, ph = lane == 0 ? Bprev : hi;
+      while (__builtin_amdgcn_ballot_w64(__double_as_longlong(pl) ==
+                                         __double_as_longlong(ph)) != ~0ull) {
+        double xl = pl, xh = ph;
+#pragma unroll
+        for (int j = 0; j < kRunMax; ++j)
+          if (j < L) {
+            xl = step(xl, dv[j]);
+            xh = step(xh, dv[j]);
+          }
+        xl = __shfl_up(xl, 1);
+        xh = __shfl_up(xh, 1);
+        if (lane > 0) {
+          pl = xl;
+          ph = xh;
         }
       }
+      // every lane from its true start, in the recurrence's own order
+      double x = pl;
+#pragma unroll
+      for (int j = 0; j < kRunMax; ++j)
+        if (j < L) {
+          x = step(x, dv[j]);
+          Bs[j * kWave + lane] = x;
+        }
+      Bprev = __shfl(x, kWave - 1);
     }
     __syncthreads();
-    for (int i = tid; i < n; i += kThreads) {
+    for (int p = tid; p < npad; p += kThreads) {
+      const int i = (p % kWave) * L + p / kWave;
+      if (i >= n) continue;
       const int s = c0 + i;
-      const int64_t kb = (int64_t)floor(Bs[i] / (double)Lb);
+      const int64_t kb = (int64_t)floor(Bs[p] / (double)Lb);
       ko[s] = (int32_t)min(kb, (int64_t)s * r);
     }
     __syncthreads();
@@ -119,7 +175,7 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(
 constexpr int kWavesPerGroup = kThreads / kWave;
 
 template <int SLOTS>
-__global__ __launch_bounds__(kThreads, SLOTS <= 32 ? 6 : 1) void topk_kernel(
+__global__ __launch_bounds__(kThreads, SLOTS <= 16 ? 8 : SLOTS <= 32 ? 6 : 1) void topk_kernel(
     const float* __restrict__ log_scores, const int32_t* __restrict__ kblocks, int64_t rows,
     int CS, int CB, int r, int kmax, int32_t* __restrict__ idx, int32_t* __restrict__ cnt) {
   // per-wave scratch: bucket counts (16-bit halves of 32-bit words: a row has
@@ -131,7 +187,7 @@ __global__ __launch_bounds__(kThreads, SLOTS <= 32 ? 6 : 1) void topk_kernel(
   if (row >= rows) return;   // no workgroup barriers below
   const int lane = threadIdx.x & (kWave - 1);
   const float* L = log_scores + row * (int64_t)CB;
-  topk::select_row<SLOTS>([&](int j) { return L[j]; }, (int)(row % CS), r, CB, kmax,
+  topk::select_row<SLOTS>([&](int j) { return L[j]; }, CB, (int)(row % CS), r, CB, kmax,
                           kblocks[row], idx + row * (int64_t)kmax, cnt + row, hist_all[wv],
                           cand_all[wv], lane);
 }
@@ -168,6 +224,8 @@ hipError_t launch_select(const float* log_scores, const float* entropy, const Se
   const int npast_max = (s.CS - 1) * s.r;
   if (npast_max <= 8 * kWave)
     return launch_topk_t<8>(log_scores, budget_blocks, s, block_idx, block_cnt, stream);
+  if (npast_max <= 16 * kWave)
+    return launch_topk_t<16>(log_scores, budget_blocks, s, block_idx, block_cnt, stream);
   if (npast_max <= 32 * kWave)
     return launch_topk_t<32>(log_scores, budget_blocks, s, block_idx, block_cnt, stream);
   if (npast_max <= 64 * kWave)

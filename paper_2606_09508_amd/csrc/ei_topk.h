@@ -3,17 +3,20 @@
 // fused probe -> select kernel (scores formed in LDS):
 //
 //   one wave per row: the row's past-block scores sit in registers as
-//   order-preserving 32-bit keys (all loads issued before any is used).  The
-//   k-th largest key T is found by radix selection: an 11-bit histogram (in
-//   LDS, 16-bit counters) of the bits below the keys' common prefix picks T's
-//   bucket (a DPP prefix sum over the lanes' 32-bucket groups, then one over
-//   the chosen group's buckets); the keys of that bucket (usually few, at
-//   most 128 here) are compacted to two per lane and T's remaining bits are
-//   resolved there with two ballots per bit.  Ties at T keep the highest
-//   block indices; the chosen blocks plus the segment's own blocks are
-//   written ascending.  The routine is bound by instruction issue: the row's
-//   index is wave-uniform and every slot loop tests its slot against the
-//   row's length as a scalar branch, so no per-slot lane masks are formed.
+//   order-preserving 32-bit keys (the loads of all the row's slots issued
+//   before any is used).  The k-th largest key T is found by radix
+//   selection: a 2048-bucket histogram (in LDS, 16-bit counters) of the
+//   keys' offsets from the row's smallest key, buckets of equal width over
+//   the row's own key range, picks T's bucket (a DPP prefix sum over the
+//   lanes' 32-bucket groups, then one over the chosen group's buckets); the
+//   keys of that bucket (usually one or two) are compacted, one or two per
+//   lane, and T is the candidate of the right rank among them (by direct
+//   comparison up to 64 candidates, else by resolving the offset's low bits
+//   with two ballots per bit).  Ties at T keep the highest block indices;
+//   the chosen blocks plus the segment's own blocks are written ascending.
+//   The row's index is wave-uniform and every slot loop tests its slot
+//   against the row's length as a scalar branch, so no per-slot lane masks
+//   are formed.
 #pragma once
 
 #include "ei_internal.h"
@@ -26,16 +29,22 @@ constexpr int kHistBins = 1 << kHistBits;
 constexpr int kHistWords = kHistBins / 2;   // 16-bit counters, two per word
 constexpr int kCandWords = 2 * kWave;        // compacted keys of T's bucket
 
-// Order-preserving key of a binary32 score, shifted by one so that 0 marks
-// an empty slot: NaN -> 1 (below -inf), -0 == +0, larger float -> larger key.
+// Order-preserving key of a binary32 score, never 0 (0 marks an empty
+// slot): NaN -> 1 (below -inf), -0 == +0, larger float -> larger key.
 // Selects only (no branches).
 __device__ __forceinline__ uint32_t score_key(float v) {
   const uint32_t u = v == 0.0f ? 0u : __float_as_uint(v);
   const uint32_t k = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-  return (v != v ? 0u : k) + 1u;   // finite/inf keys are <= 0xff800000, so no wrap
+  return v != v ? 1u : k;   // finite / inf keys are >= 0x007fffff (-inf)
 }
 
 __device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
+
+// The number of set bits of the wave mask m below this lane.
+__device__ __forceinline__ int rank_below(uint64_t m) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                        __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
 
 // A copy of a wave-uniform value that the optimizer cannot see through: the
 // slot tests of each loop against it stay scalar branches, instead of lane
@@ -52,18 +61,19 @@ __device__ __forceinline__ void wave_lds_fence() {
 }
 
 // One row, by the whole wave (every argument wave-uniform but `lane`):
-// `score(j)` is the binary32 score of past block j < npast = s r; kk = k_s
+// `score(j)` is the binary32 score of past block j < npast = s r, and may be
+// read for every j < avail (its values past npast are not used); kk = k_s
 // blocks are kept (kk >= npast keeps all of them), then the segment's own
 // blocks s r .. min((s+1) r, C_B) - 1; out receives kmax entries, ascending,
 // -1 padded, and *cnt the count.  hist (kHistWords words) and cand
 // (kCandWords words) are this wave's LDS scratch.
 template <int SLOTS, class Score>
-__device__ __forceinline__ void select_row(Score score, int s, int r, int CB, int kmax, int kk,
+__device__ __forceinline__ void select_row(Score score, int avail, int s, int r, int CB, int kmax,
+                                           int kk,
                                            int32_t* __restrict__ out, int32_t* __restrict__ cnt,
                                            uint32_t* hist, uint32_t* cand, int lane) {
   const int npast = s * r;
   const int nsl = (npast + kWave - 1) / kWave;
-  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   int pos = 0;
 
   if (kk >= npast) {
@@ -71,21 +81,47 @@ __device__ __forceinline__ void select_row(Score score, int s, int r, int CB, in
     pos = npast;
   } else if (kk > 0) {
     uint32_t key[SLOTS];
-    uint32_t kmx = 0, kmn = 0xffffffffu;
-    // all loads first, unconditionally (lanes past the row read its last
-    // past block, one shared line), so that they are in flight together
+    uint32_t kmx = 0, kmn1 = 0xffffffffu;   // kmn1: the smallest non-empty key - 1
+    // the loads of the row's slots first, in groups of kG slots, so that
+    // they are in flight together; lanes past the row read unused values
+    // (past npast, or its last past block where the groups reach past avail)
     float raw[SLOTS];
+    constexpr int kG = SLOTS <= 8 ? SLOTS : 8;
+    const int nsr = SLOTS <= kG ? 1 : fresh_uniform(nsl);
+    if ((nsl + kG - 1) / kG * kG * kWave <= avail) {
+      // every slot of the groups loaded is readable: no clamp
 #pragma unroll
-    for (int sl = 0; sl < SLOTS; ++sl) raw[sl] = score(min(sl * kWave + lane, npast - 1));
+      for (int g = 0; g < SLOTS; g += kG)
+        if (g < nsr) {
 #pragma unroll
-    for (int sl = 0; sl < SLOTS; ++sl) {
-      const int j = sl * kWave + lane;
-      key[sl] = j < npast ? score_key(raw[sl]) : 0u;   // j < npast: sl < nsl
-      kmx = key[sl] > kmx ? key[sl] : kmx;
-      kmn = (key[sl] != 0u && key[sl] < kmn) ? key[sl] : kmn;
+          for (int sl = g; sl < g + kG; ++sl) raw[sl] = score(sl * kWave + lane);
+        }
+    } else {
+#pragma unroll
+      for (int g = 0; g < SLOTS; g += kG)
+        if (g < nsr) {
+#pragma unroll
+          for (int sl = g; sl < g + kG; ++sl) raw[sl] = score(min(sl * kWave + lane, npast - 1));
+        }
+    }
+    const int nsk = SLOTS <= kG ? 1 : fresh_uniform(nsl);
+#pragma unroll
+    for (int g = 0; g < SLOTS; g += kG) {
+      if (g < nsk) {
+#pragma unroll
+        for (int sl = g; sl < g + kG; ++sl) {
+          const uint32_t k = score_key(raw[sl]);
+          key[sl] = (uint32_t)(sl * kWave + lane - npast) >> 31 ? k : 0u;   // j < npast
+          kmx = key[sl] > kmx ? key[sl] : kmx;
+          kmn1 = min(kmn1, key[sl] - 1u);   // an empty slot's 0 wraps to the maximum
+        }
+      } else {
+#pragma unroll
+        for (int sl = g; sl < g + kG; ++sl) key[sl] = 0u;
+      }
     }
     kmx = wave_max_u32_f(kmx);
-    kmn = wave_min_u32_f(kmn);
+    const uint32_t kmn = wave_min_u32_f(kmn1) + 1u;
     // T = the kk-th largest key; gt / eq = keys above / equal to T.
     uint32_t T;
     int gt = -1, eq = -1;
@@ -94,20 +130,19 @@ __device__ __forceinline__ void select_row(Score score, int s, int r, int CB, in
       gt = 0;
       eq = npast;
     } else {
-      // Valid keys share the bits above `top`; bucket them by the next
-      // (up to) 11 bits.
-      const int top = 31 - __clz(kmx ^ kmn);
-      const uint32_t prefix = kmx & ~((top == 31) ? 0xffffffffu : ((2u << top) - 1u));
-      const int shift = max(top - (kHistBits - 1), 0);
-      const uint32_t dmask = (2u << (top - shift)) - 1u;
+      // Bucket the keys by their offset from the smallest, (key - kmn) >>
+      // shift < 2^11: buckets of equal width over the row's own key range.
+      const int shift = max(32 - __clz(kmx - kmn) - kHistBits, 0);
       for (int i = lane; i < kHistBins / 8; i += kWave) ((uint4*)hist)[i] = make_uint4(0, 0, 0, 0);
       wave_lds_fence();
       const int nsh = fresh_uniform(nsl);
 #pragma unroll
       for (int sl = 0; sl < SLOTS; ++sl)
         if (sl < nsh && key[sl]) {
-          const uint32_t bin = (key[sl] >> shift) & dmask;
-          atomicAdd(&hist[bin >> 1], 1u << (16 * (bin & 1)));
+          // bucket (key - kmn) >> shift: half (bucket & 1) of word bucket >> 1
+          const uint32_t d = key[sl] - kmn;
+          const uint32_t half = __builtin_amdgcn_ubfe(d, (uint32_t)shift, 1u);
+          atomicAdd(&hist[d >> (shift + 1)], __umul24(half, 0xffffu) + 1u);   // 1 or 1 << 16
         }
       wave_lds_fence();
       // Lane l owns buckets 32 l .. 32 l + 31; find the bucket holding T from
@@ -139,43 +174,68 @@ __device__ __forceinline__ void select_row(Score score, int s, int r, int CB, in
       const int dstar = 32 * ls + 31 - tb;
       const uint32_t above = acc0 + rl_u32(run - bt, tb);
       const uint32_t nb = rl_u32(bt, tb);
-      T = prefix | ((uint32_t)dstar << shift);
+      // T = kmn + Toff; Toff's bits below `shift` are resolved from the top
+      uint32_t Toff = (uint32_t)dstar << shift;
       if (shift == 0) {
+        T = kmn + Toff;
         gt = (int)above;
         eq = (int)nb;
       } else if (nb <= (uint32_t)(2 * kWave)) {
         // compact the bucket's keys, two per lane, and resolve the low bits
+        // the bucket's keys are those in [blo, bhi] (an empty slot's 0 is
+        // below blo >= kmn >= 1)
+        const uint32_t blo = kmn + Toff, bhi = blo + ((1u << shift) - 1u);
         int cp = 0;
         const int nsc = fresh_uniform(nsl);
 #pragma unroll
         for (int sl = 0; sl < SLOTS; ++sl) {
           if (sl < nsc) {
-            const bool in = key[sl] != 0u && ((key[sl] >> shift) & dmask) == (uint32_t)dstar;
+            const bool in = key[sl] >= blo && key[sl] <= bhi;
             const uint64_t m = ballot(in);
-            if (in) cand[cp + popc64(m & lt_mask)] = key[sl];
-            cp += popc64(m);
+            if (m != 0) {
+              if (in) cand[(uint32_t)(cp + rank_below(m))] = key[sl];
+              cp += popc64(m);
+            }
           }
         }
         wave_lds_fence();
         const uint32_t c0 = lane < (int)nb ? cand[lane] : 0u;
+        if (nb <= (uint32_t)kWave) {
+          // one candidate per lane: T is the one with fewer than `need`
+          // candidates above it and at least `need` at or above it
+          const int need = kk - (int)above;   // 1 .. nb
+          int ngt = 0, nge = 0;
+          for (int t = 0; t < (int)nb; ++t) {
+            const uint32_t x = cand[t];   // the same word for every lane
+            ngt += x > c0 ? 1 : 0;
+            nge += x >= c0 ? 1 : 0;
+          }
+          const uint64_t hm = ballot(lane < (int)nb && ngt < need && need <= nge);
+          T = rl_u32(c0, (int)__builtin_ctzll(hm));
+          gt = (int)above + popc64(ballot(c0 > T));
+          eq = popc64(ballot(c0 == T));
+        } else {
         const uint32_t c1 = lane + kWave < (int)nb ? cand[lane + kWave] : 0u;
         for (int bit = shift - 1; bit >= 0; --bit) {
-          const uint32_t c = T | (1u << bit);
-          if ((int)above + popc64(ballot(c0 >= c)) + popc64(ballot(c1 >= c)) >= kk) T = c;
+          const uint32_t co = Toff | (1u << bit), c = kmn + co;   // empty (0) is below c
+          if ((int)above + popc64(ballot(c0 >= c)) + popc64(ballot(c1 >= c)) >= kk) Toff = co;
         }
+        T = kmn + Toff;
         gt = (int)above + popc64(ballot(c0 > T)) + popc64(ballot(c1 > T));
         eq = popc64(ballot(c0 == T)) + popc64(ballot(c1 == T));
+        }
       } else {
-        // large bucket (many equal high bits): resolve over all slots
+        // large bucket (many keys of nearly one value): resolve over all slots
         for (int bit = shift - 1; bit >= 0; --bit) {
-          const uint32_t c = T | (1u << bit);
+          const uint32_t co = Toff | (1u << bit), c = kmn + co;
           int n = 0;
           const int nsb = fresh_uniform(nsl);
 #pragma unroll
           for (int sl = 0; sl < SLOTS; ++sl)
             if (sl < nsb) n += popc64(ballot(key[sl] >= c));
-          if (n >= kk) T = c;
+          if (n >= kk) Toff = co;
         }
+        T = kmn + Toff;
       }
     }
     if (gt < 0) {
@@ -227,7 +287,7 @@ __device__ __forceinline__ void select_row(Score score, int s, int r, int CB, in
         if (sl < nsp) {
           const bool pick = key[sl] >= T;
           const uint64_t m = ballot(pick);
-          if (pick) out[pos + popc64(m & lt_mask)] = sl * kWave + lane;
+          if (pick) out[(uint32_t)(pos + rank_below(m))] = sl * kWave + lane;
           pos += popc64(m);
         }
       }
@@ -238,7 +298,7 @@ __device__ __forceinline__ void select_row(Score score, int s, int r, int CB, in
           const int j = sl * kWave + lane;
           const bool pick = key[sl] > T || (key[sl] == T && j >= J);
           const uint64_t m = ballot(pick);
-          if (pick) out[pos + popc64(m & lt_mask)] = j;
+          if (pick) out[(uint32_t)(pos + rank_below(m))] = j;
           pos += popc64(m);
         }
       }

@@ -527,6 +527,42 @@ def test_budget_recurrence_across_chunks():
         np.testing.assert_array_equal(g[name], ref[name], err_msg=name)
 
 
+def test_budget_recurrence_off_the_clamps():
+    """Alg. 3's recurrence where the budget stays strictly between B_h and
+    3 B_h for a whole chunk of segments (entropy ratios within 0.005 of
+    Delta_t, so every increment is a few tokens), so no run of steps can be
+    settled without the value carried into it and the kernel's evaluation
+    degenerates to the sequential order; head 1 mixes such stretches with
+    clamped ones.  1324 segments, so the unclamped value is also carried
+    across a chunk boundary.  Budgets, counts and lists bit-exact against the
+    oracle."""
+    Ls, Lb, Hq = 128, 64, 2
+    CS = 1024 + 300
+    N, CB = CS * Ls, 2 * CS
+    rng = np.random.default_rng(23)
+    en = np.empty((1, Hq, CS), np.float64)
+    for h, (ulo, uhi) in enumerate([(0.395, 0.405), (0.2, 0.6)]):
+        e = [1.0, 3.4]                            # ratio 2.4: B_1 = B_h + 2 alpha B_h
+        for _ in range(CS - 2):
+            u = rng.uniform(ulo, uhi)
+            e.append(e[-1] * (1.0 - u if e[-1] > 1.0 else 1.0 + u))
+        en[0, h] = e
+    en[0, 1, 700:720] = en[0, 1, 699]             # flat run: down to B_h
+    en = en.astype(np.float32)
+    ls = rng.standard_normal((1, Hq, CS, CB)).astype(np.float32)
+    sel = eb.select_blocks(torch.from_numpy(ls).cuda(), torch.from_numpy(en).cuda(), N, Ls, Lb,
+                           1e-5, 0.5, 0.4, 2048, 3, n_kv_heads=1)
+    torch.cuda.synchronize()
+    g = {kk: t.cpu().numpy() for kk, t in sel.items()}
+    ref = oracle.select(ls, en, N, Ls, Lb, 1e-5, 0.5, 0.4, 2048, 3)
+    b = ref["budget"][0]
+    assert not ref["rigid"].any()
+    assert (b[0, 48:] > 32).all() and (b[0, 48:] < 96).all()    # never clamped
+    assert (b[1, 48:] == 32).any() and (b[1, 48:] == 96).any() and len(np.unique(b[1, 48:])) > 20
+    for name in ("rigid", "budget", "cnt", "idx"):
+        np.testing.assert_array_equal(g[name], ref[name], err_msg=name)
+
+
 @pytest.mark.parametrize("mode", [eb.CLASSIFY_HEAD, eb.CLASSIFY_GQA_GROUP, eb.CLASSIFY_SEGMENT])
 @pytest.mark.parametrize("e_t", [1e-5, math.inf])
 def test_select_modes_match_oracle(mode, e_t):
