@@ -38,38 +38,76 @@ constexpr int kThreads = 256;
 constexpr int kChunk = 1024;
 constexpr int kRunMax = kChunk / kWave;   // steps per lane in the budget recurrence
 
+// Lane l receives lane l - 1's v (lane 0 keeps its own): a DPP wave shift.
+__device__ __forceinline__ double shift_up1(double v) {
+  const int2 w = __builtin_bit_cast(int2, v);
+  const int lo = __builtin_amdgcn_update_dpp(w.x, w.x, 0x138, 0xf, 0xf, false);   // wave_shr:1
+  const int hi = __builtin_amdgcn_update_dpp(w.y, w.y, 0x138, 0xf, 0xf, false);
+  return __builtin_bit_cast(double, make_int2(lo, hi));
+}
+
+template <bool GROUP>
 __global__ __launch_bounds__(kThreads) void budget_kernel(
     const float* __restrict__ entropy, int Hq, int CS, int r, int Lb, float e_t, double alpha,
     double delta_t, int Bh, int mult, int mode, int G, uint8_t* __restrict__ rigid_out,
     int32_t* __restrict__ k_out) {
   __shared__ double delta[kChunk];   // -inf: the segment restarts at B_h
   __shared__ double Bs[kChunk];
-  __shared__ float ent[kChunk];      // E(c0 + i) of the chunk at c0
   const int64_t bh = blockIdx.x;
   int32_t* ko = k_out + bh * CS;
   const int tid = threadIdx.x;
   // the entropy row this head's budgets follow
-  const bool group = mode == EI_CLASSIFY_GQA_GROUP;
-  const float* e = entropy + (group ? bh - (bh % Hq) % G : bh) * CS;
+  const float* e = entropy + (GROUP ? bh - (bh % Hq) % G : bh) * CS;
   auto E = [&](int s) -> float {
-    if (!group) return e[s];
-    double sum = 0.0;
-    for (int h = 0; h < G; ++h) sum += (double)e[(int64_t)h * CS + s];
-    return (float)(sum / (double)G);
+    if constexpr (!GROUP) {
+      return e[s];
+    } else {
+      double sum = 0.0;
+      for (int h = 0; h < G; ++h) sum += (double)e[(int64_t)h * CS + s];
+      return (float)(sum / (double)G);
+    }
   };
 
-  // the rigid test over every segment, keeping the first chunk's entropies
-  int below = 1;
-#pragma unroll 4
-  for (int s = tid; s < CS; s += kThreads) {
-    const float v = E(s);
-    if (s < kChunk) ent[s] = v;
-    if (!(v < e_t)) below = 0;
-  }
-  below = __syncthreads_and(below);
   const double B0 = (double)Bh;
   const double cap = (double)mult * B0;
   const double a = alpha * B0;
+  // The increments of the chunk of steps at c0 (n steps) into delta.  The
+  // steps are padded with zero increments to a whole number of waves (a zero
+  // increment leaves a clamped value unchanged) and split into kWave runs of
+  // L consecutive steps; step i = l L + j of lane l's run is held at
+  // delta[j kWave + l], so every lane's reads and writes of a step are one
+  // conflict-free row.  Up to four steps per thread, with selects rather
+  // than branches so that their loads issue together (a padding step reads
+  // an unused segment).  Returns 0 if a segment of the chunk is not below
+  // e_t.
+  auto increments = [&](int c0, int n) {
+    const int npad = (n + kWave - 1) / kWave * kWave;
+    const int L = npad / kWave;
+    int low = 1;
+#pragma unroll 4
+    for (int p = tid; p < npad; p += kThreads) {
+      const int i = (p % kWave) * L + p / kWave;
+      const int s = c0 + min(i, n - 1);
+      const float es = E(s), eprev = E(max(s - 1, 0));
+      if (!(es < e_t)) low = 0;
+      const double ep = (double)eprev, ec = (double)es;
+      const double num = fabs(ec - ep);
+      const double ratio = (num == 0.0 && ep == 0.0) ? 0.0 : num / ep;
+      double d = a * (ratio - delta_t);
+      // B_0 = B_h, and a rigid segment of the per-segment rule takes B_h:
+      // B_prev + (-inf) is clamped to exactly B_h below
+      d = (s == 0 || (mode == EI_CLASSIFY_SEGMENT && es < e_t)) ? -INFINITY : d;
+      delta[p] = i < n ? d : 0.0;
+    }
+    return low;
+  };
+
+  // the rigid test over every segment, the first chunk's increments on the way
+  int below = increments(0, min(kChunk, CS));
+#pragma unroll 4
+  for (int s = kChunk + tid; s < CS; s += kThreads)
+    if (!(E(s) < e_t)) below = 0;
+  below = __syncthreads_and(below);
   if (tid == 0) rigid_out[bh] = (uint8_t)(below ? 1 : 0);
   if (below) {
     const int64_t kb = (int64_t)floor(B0 / (double)Lb);
@@ -80,37 +118,8 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(
   double Bprev = B0;   // wave 0: B before the chunk's first step
   for (int c0 = 0; c0 < CS; c0 += kChunk) {
     const int n = min(kChunk, CS - c0);
-    // The steps are padded with zero increments to a whole number of waves
-    // (a zero increment leaves a clamped value unchanged) and split into
-    // kWave runs of L consecutive steps; step i = l L + j of lane l's run is
-    // held at delta[j kWave + l], so every lane's reads and writes of a step
-    // are one conflict-free row.
-    const int npad = (n + kWave - 1) / kWave * kWave;
-    const int L = npad / kWave;
-    if (c0 > 0) {
-      for (int i = tid; i < n; i += kThreads) ent[i] = E(c0 + i);
-      __syncthreads();
-    }
-    for (int p = tid; p < npad; p += kThreads) {
-      const int i = (p % kWave) * L + p / kWave;
-      if (i >= n) {
-        delta[p] = 0.0;
-        continue;
-      }
-      const int s = c0 + i;
-      const float es = ent[i];
-      // B_0 = B_h, and a rigid segment of the per-segment rule takes B_h:
-      // B_prev + (-inf) is clamped to exactly B_h below
-      if (s == 0 || (mode == EI_CLASSIFY_SEGMENT && es < e_t)) {
-        delta[p] = -INFINITY;
-        continue;
-      }
-      const double ep = (double)(i > 0 ? ent[i - 1] : E(s - 1)), ec = (double)es;
-      const double num = fabs(ec - ep);
-      const double ratio = (num == 0.0 && ep == 0.0) ? 0.0 : num / ep;
-      const double t = ratio - delta_t;
-      delta[p] = a * t;
-    }
+    const int L = (n + kWave - 1) / kWave, npad = L * kWave;
+    if (c0 > 0) increments(c0, n);   // the first chunk's are in delta already
     __syncthreads();
     if (tid < kWave) {
       // One step of the recurrence.  The clamps as fmax / fmin give the same
@@ -143,8 +152,8 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(
             xl = step(xl, dv[j]);
             xh = step(xh, dv[j]);
           }
-        xl = __shfl_up(xl, 1);
-        xh = __shfl_up(xh, 1);
+        xl = shift_up1(xl);
+        xh = shift_up1(xh);
         if (lane > 0) {
           pl = xl;
           ph = xh;
@@ -210,9 +219,14 @@ bool select_supported(const SelectShape& s) { return s.CB <= 128 * kWave; }
 
 hipError_t launch_budget(const float* entropy, const SelectShape& s, uint8_t* rigid,
                          int32_t* budget_blocks, hipStream_t stream) {
-  hipLaunchKernelGGL(budget_kernel, dim3((unsigned)(s.B * s.Hq)), dim3(kThreads), 0, stream,
-                     entropy, s.Hq, s.CS, s.r, s.Lb, s.e_t, s.alpha, s.delta_t, s.Bh, s.mult,
-                     s.mode, s.G, rigid, budget_blocks);
+  if (s.mode == EI_CLASSIFY_GQA_GROUP)
+    hipLaunchKernelGGL(budget_kernel<true>, dim3((unsigned)(s.B * s.Hq)), dim3(kThreads), 0,
+                       stream, entropy, s.Hq, s.CS, s.r, s.Lb, s.e_t, s.alpha, s.delta_t, s.Bh,
+                       s.mult, s.mode, s.G, rigid, budget_blocks);
+  else
+    hipLaunchKernelGGL(budget_kernel<false>, dim3((unsigned)(s.B * s.Hq)), dim3(kThreads), 0,
+                       stream, entropy, s.Hq, s.CS, s.r, s.Lb, s.e_t, s.alpha, s.delta_t, s.Bh,
+                       s.mult, s.mode, s.G, rigid, budget_blocks);
   return hipGetLastError();
 }
 
