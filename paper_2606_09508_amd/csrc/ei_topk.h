@@ -107,7 +107,15 @@ __device__ __forceinline__ void select_row(Score score, int avail, int s, int r,
     const int nsk = SLOTS <= kG ? 1 : fresh_uniform(nsl);
 #pragma unroll
     for (int g = 0; g < SLOTS; g += kG) {
-      if (g < nsk) {
+      if (g + kG < nsk) {
+        // every slot of the group is full (only the row's last slot is not)
+#pragma unroll
+        for (int sl = g; sl < g + kG; ++sl) {
+          key[sl] = score_key(raw[sl]);
+          kmx = key[sl] > kmx ? key[sl] : kmx;
+          kmn1 = min(kmn1, key[sl] - 1u);
+        }
+      } else if (g < nsk) {
 #pragma unroll
         for (int sl = g; sl < g + kG; ++sl) {
           const uint32_t k = score_key(raw[sl]);
@@ -136,14 +144,23 @@ __device__ __forceinline__ void select_row(Score score, int avail, int s, int r,
       for (int i = lane; i < kHistBins / 8; i += kWave) ((uint4*)hist)[i] = make_uint4(0, 0, 0, 0);
       wave_lds_fence();
       const int nsh = fresh_uniform(nsl);
+      auto count = [&](uint32_t kv) {
+        // bucket (kv - kmn) >> shift: half (bucket & 1) of word bucket >> 1
+        const uint32_t d = kv - kmn;
+        const uint32_t half = __builtin_amdgcn_ubfe(d, (uint32_t)shift, 1u);
+        atomicAdd(&hist[d >> (shift + 1)], __umul24(half, 0xffffu) + 1u);   // 1 or 1 << 16
+      };
 #pragma unroll
-      for (int sl = 0; sl < SLOTS; ++sl)
-        if (sl < nsh && key[sl]) {
-          // bucket (key - kmn) >> shift: half (bucket & 1) of word bucket >> 1
-          const uint32_t d = key[sl] - kmn;
-          const uint32_t half = __builtin_amdgcn_ubfe(d, (uint32_t)shift, 1u);
-          atomicAdd(&hist[d >> (shift + 1)], __umul24(half, 0xffffu) + 1u);   // 1 or 1 << 16
+      for (int g = 0; g < SLOTS; g += kG) {
+        if (g + kG < nsh) {
+#pragma unroll
+          for (int sl = g; sl < g + kG; ++sl) count(key[sl]);   // full slots
+        } else if (g < nsh) {
+#pragma unroll
+          for (int sl = g; sl < g + kG; ++sl)
+            if (sl < nsh && key[sl]) count(key[sl]);
         }
+      }
       wave_lds_fence();
       // Lane l owns buckets 32 l .. 32 l + 31; find the bucket holding T from
       // the top: the largest d with (keys in buckets >= d) >= kk.

@@ -527,7 +527,8 @@ def test_budget_recurrence_across_chunks():
         np.testing.assert_array_equal(g[name], ref[name], err_msg=name)
 
 
-def test_budget_recurrence_off_the_clamps():
+@pytest.mark.parametrize("mode", [eb.CLASSIFY_HEAD, eb.CLASSIFY_GQA_GROUP, eb.CLASSIFY_SEGMENT])
+def test_budget_recurrence_off_the_clamps(mode):
     """Alg. 3's recurrence where the budget stays strictly between B_h and
     3 B_h for a whole chunk of segments (entropy ratios within 0.005 of
     Delta_t, so every increment is a few tokens), so no run of steps can be
@@ -535,7 +536,8 @@ def test_budget_recurrence_off_the_clamps():
     degenerates to the sequential order; head 1 mixes such stretches with
     clamped ones.  1324 segments, so the unclamped value is also carried
     across a chunk boundary.  Budgets, counts and lists bit-exact against the
-    oracle."""
+    oracle, under each classification rule (the GQA-group rule follows the
+    two heads' mean)."""
     Ls, Lb, Hq = 128, 64, 2
     CS = 1024 + 300
     N, CB = CS * Ls, 2 * CS
@@ -551,16 +553,18 @@ def test_budget_recurrence_off_the_clamps():
     en = en.astype(np.float32)
     ls = rng.standard_normal((1, Hq, CS, CB)).astype(np.float32)
     sel = eb.select_blocks(torch.from_numpy(ls).cuda(), torch.from_numpy(en).cuda(), N, Ls, Lb,
-                           1e-5, 0.5, 0.4, 2048, 3, n_kv_heads=1)
+                           1e-5, 0.5, 0.4, 2048, 3, n_kv_heads=1, mode=mode)
     torch.cuda.synchronize()
     g = {kk: t.cpu().numpy() for kk, t in sel.items()}
-    ref = oracle.select(ls, en, N, Ls, Lb, 1e-5, 0.5, 0.4, 2048, 3)
+    ref = oracle.select(ls, en, N, Ls, Lb, 1e-5, 0.5, 0.4, 2048, 3, mode=mode, n_kv_heads=1)
     b = ref["budget"][0]
     assert not ref["rigid"].any()
-    assert (b[0, 48:] > 32).all() and (b[0, 48:] < 96).all()    # never clamped
-    assert (b[1, 48:] == 32).any() and (b[1, 48:] == 96).any() and len(np.unique(b[1, 48:])) > 20
+    if mode != eb.CLASSIFY_GQA_GROUP:
+        assert (b[0, 48:] > 32).all() and (b[0, 48:] < 96).all()    # never clamped
+        assert (b[1, 48:] == 32).any() and (b[1, 48:] == 96).any()
+        assert len(np.unique(b[1, 48:])) > 20
     for name in ("rigid", "budget", "cnt", "idx"):
-        np.testing.assert_array_equal(g[name], ref[name], err_msg=name)
+        np.testing.assert_array_equal(g[name], ref[name], err_msg=f"{name} mode={mode}")
 
 
 @pytest.mark.parametrize("mode", [eb.CLASSIFY_HEAD, eb.CLASSIFY_GQA_GROUP, eb.CLASSIFY_SEGMENT])
