@@ -28,6 +28,7 @@ constexpr int kHistBits = 11;
 constexpr int kHistBins = 1 << kHistBits;
 constexpr int kHistWords = kHistBins / 2;   // 16-bit counters, two per word
 constexpr int kCandWords = 2 * kWave;        // compacted keys of T's bucket
+static_assert(kHistBins % (8 * kWave) == 0, "the histogram is cleared 16 bytes per lane at a time");
 
 // Order-preserving key of a binary32 score, never 0 (0 marks an empty
 // slot): NaN -> 1 (below -inf), -0 == +0, larger float -> larger key.
@@ -141,7 +142,9 @@ __device__ __forceinline__ void select_row(Score score, int avail, int s, int r,
       // Bucket the keys by their offset from the smallest, (key - kmn) >>
       // shift < 2^11: buckets of equal width over the row's own key range.
       const int shift = max(32 - __clz(kmx - kmn) - kHistBits, 0);
-      for (int i = lane; i < kHistBins / 8; i += kWave) ((uint4*)hist)[i] = make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int i = 0; i < kHistBins / 8 / kWave; ++i)
+        ((uint4*)hist)[i * kWave + lane] = make_uint4(0, 0, 0, 0);
       wave_lds_fence();
       const int nsh = fresh_uniform(nsl);
       auto count = [&](uint32_t kv) {
