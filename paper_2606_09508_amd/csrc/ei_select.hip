@@ -6,12 +6,15 @@
 //                 parallel, the clamped budget recurrence and
 //                 k_s = min(floor(B_s / L_B), s r).  The recurrence runs in
 //                 one wave, each lane owning a run of consecutive steps:
-//                 since one step x -> min(max(x + d, B_h), 3 B_h) is
-//                 monotone, a run evaluated from both ends of the clamp range
-//                 gives the true value wherever the two evaluations meet, so
-//                 a lane whose predecessor's run met knows its start at once;
-//                 the others wait for their predecessor, which is the
-//                 sequential order in the worst case.
+//                 since one step x -> min(max(x + d, B_h), m B_h) is
+//                 monotone, a run evaluated from both ends of an interval
+//                 holding its true start bounds its true values.  Each round
+//                 every lane runs its steps from both ends of its interval
+//                 and hands the two ends reached to the next lane; an
+//                 interval that has shrunk to one value is the true start.
+//                 Runs that meet a clamp from both ends settle the next lane
+//                 at once, and after at most 63 rounds every start is known
+//                 (the sequential order, in the worst case).
 //                 Variants: the entropies may be the GQA group's means
 //                 (binary64 sum in head order / G, rounded to binary32), and
 //                 the rigid rule may apply per segment (B_s = B_h wherever
@@ -124,7 +127,7 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(
     if (tid < kWave) {
       // One step of the recurrence.  The clamps as fmax / fmin give the same
       // value as the comparisons in every case (NaN and -inf -> B_h, +inf ->
-      // 3 B_h), and every value a step yields lies in [lo, hi].
+      // m B_h), and every value a step yields lies in [lo, hi].
       auto step = [&](double x, double d) { return fmin(fmax(x + d, B0), cap); };
       const double lo = step(B0, -INFINITY), hi = step(B0, INFINITY);
       const int lane = tid;
