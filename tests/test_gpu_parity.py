@@ -480,13 +480,15 @@ def _crafted_large_scores(CS, CB, seed=7):
     return ls, en
 
 
-@pytest.mark.parametrize("N", [131072, 524288])
+@pytest.mark.parametrize("N", [65472, 65536, 131008, 131072, 262144, 524288])
 def test_select_crafted_large_rows(N):
-    """The 32- and 128-slot selector instances, bit-exact against the oracle
-    on crafted rows (large threshold buckets, ties at T, NaN / inf / +-0),
-    with budgets that keep 32..96 and up to 384 past blocks."""
+    """The 16-, 32-, 64- and 128-slot selector instances, bit-exact against
+    the oracle on crafted rows (large threshold buckets, ties at T, NaN / inf
+    / +-0), with budgets that keep 32..96 and up to 384 past blocks.  C_B =
+    1023 and 2047 (N not a multiple of 64 blocks' rows) make the long rows'
+    slot groups reach past the row, where the loads are clamped."""
     Ls, Lb = 128, 64
-    CS, CB = N // Ls, N // Lb
+    CS, CB = -(-N // Ls), -(-N // Lb)
     ls, en = _crafted_large_scores(CS, CB)
     for bh, mult in ((2048, 3), (8192, 3)):
         sel = eb.select_blocks(torch.from_numpy(ls).cuda(), torch.from_numpy(en).cuda(), N, Ls,
